@@ -1,0 +1,207 @@
+/*
+ * ippd.h -- C ABI of the MI355X (gfx950) library for the decode step of
+ * Intra-Prompt Parallel Decoding (IPPD, arXiv 2609.05707).
+ *
+ * In IPPD the questions that share a context are stacked into one prompt
+ * and decoded in parallel (Sec. 4).  At a decode step every still-active
+ * question feeds one token; that token's query attends to
+ *   - the shared context of its prompt (instruction + context; the mask
+ *     clauses M_ctx and M_caus of Sec. 4.1 admit all of it), and
+ *   - its own question+answer segment, including the token itself
+ *     (M_qtn and M_caus with ">=", Sec. 4.1),
+ * and to nothing else.  The token sits at virtual position
+ * |p| + |c_j| + |x_jk| + (t-1) (Sec. 4.1), i.e. the context length plus the
+ * number of segment tokens already cached.  The result equals independent
+ * causal decoding of each question (Sec. 4.2).  Prompts of a batch carry
+ * different contexts and question counts; stopped questions take no token
+ * and produce no output (Sec. 4.2 end-of-sequence rule, Sec. 4.4 pads).
+ *
+ * Conventions for every entry point:
+ *   - Array arguments are DEVICE pointers unless marked "host".  All work is
+ *     enqueued on `stream`; no entry point synchronises, allocates or frees.
+ *     The caller owns every buffer.  Calls that share buffers must be
+ *     ordered on one stream.
+ *   - Host-checkable argument errors return a status before anything is
+ *     enqueued.  Problems only visible in device data (see IPPD_FLAG_*) are
+ *     reported by OR-ing bits into *err_flag; affected rows are skipped.
+ *   - Rotary embedding: rotate-half pairs (j, j + D/2) with
+ *     theta_j = rope_base^(-2j/D); the angle pos*theta_j is formed in fp64.
+ *   - Softmax scale 1/sqrt(D) unless `scale` > 0 (Sec. 4.2).
+ *   - GQA: query head h reads kv head h / (Hq/Hkv).
+ */
+#ifndef IPPD_H
+#define IPPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  IPPD_DTYPE_F32 = 0,   /* float32 cache and q/k/v */
+  IPPD_DTYPE_BF16 = 1   /* bfloat16 cache and q/k/v; fp32 accumulation */
+} ippd_dtype_t;
+
+typedef enum {
+  IPPD_OK = 0,
+  IPPD_ERR_NULL = 1,       /* a required pointer is NULL */
+  IPPD_ERR_SHAPE = 2,      /* inconsistent or unsupported sizes */
+  IPPD_ERR_DTYPE = 3,      /* unknown dtype */
+  IPPD_ERR_ALIGN = 4,      /* a data pointer is not 16-byte aligned */
+  IPPD_ERR_WORKSPACE = 5,  /* workspace NULL or smaller than required */
+  IPPD_ERR_HIP = 6         /* a HIP launch failed; see ippd_last_hip_error() */
+} ippd_status_t;
+
+/* Bits OR-ed into *err_flag by device code. */
+#define IPPD_FLAG_SEGMENT_FULL 1  /* append found seg_len[i] == seg_capacity: token dropped */
+#define IPPD_FLAG_BAD_LAYOUT   2  /* device arrays break a rule below: rows skipped */
+
+/*
+ * Batch description (a host struct; its array fields are device pointers).
+ *
+ * Prompts b = 0..B-1.  Prompt b's context occupies tokens
+ * [ctx_off[b], ctx_off[b] + ctx_len[b]) of the context pool; ctx_off[b] must
+ * be a multiple of 8 and the range must lie inside [0, ctx_pool_tokens).
+ * Its questions are i = q_start[b] .. q_start[b+1]-1 (q_start[0] = 0,
+ * q_start[B] = num_questions, non-decreasing).  Question i owns one segment
+ * per kv head holding seg_len[i] <= seg_capacity cached tokens (question +
+ * answer tokens so far) at virtual positions ctx_len[b] + 0..seg_len[i]-1.
+ * active[i] != 0 marks a question still decoding this step.
+ * max_ctx_len >= every ctx_len[b] and max_questions >= every question count
+ * are host-side bounds used to size grids and workspaces (violations set
+ * IPPD_FLAG_BAD_LAYOUT).
+ */
+typedef struct ippd_batch {
+  int32_t num_prompts;       /* B >= 1 */
+  int32_t num_questions;     /* Nt >= 0, total over prompts */
+  int32_t num_q_heads;       /* Hq >= 1 */
+  int32_t num_kv_heads;      /* Hkv >= 1, Hq % Hkv == 0, Hq/Hkv <= 64 */
+  int32_t head_dim;          /* D: 64 or 128 */
+  int32_t dtype;             /* ippd_dtype_t */
+  int64_t ctx_pool_tokens;   /* context pool capacity, multiple of 8 */
+  int32_t seg_capacity;      /* tokens per segment, multiple of 8, >= 8 */
+  int32_t max_ctx_len;       /* host bound on ctx_len[b], <= ctx_pool_tokens */
+  int32_t max_questions;     /* host bound on questions per prompt, 1..1024 */
+  int32_t chunk_tokens;      /* context tokens per work unit: 0 = automatic,
+                                else a multiple of 32 (tests use it to vary splits) */
+  double  rope_base;         /* > 0, e.g. 10000 */
+  float   scale;             /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
+  const int64_t *ctx_off;    /* [B]   pool offset of each context */
+  const int32_t *ctx_len;    /* [B]   context tokens per prompt (|p| + |c_j|) */
+  const int32_t *q_start;    /* [B+1] question CSR offsets */
+  int32_t       *seg_len;    /* [Nt]  cached segment tokens; advanced by ippd_append_kv */
+  const uint8_t *active;     /* [Nt]  1 = decoding this step */
+  int32_t       *err_flag;   /* [1]   IPPD_FLAG_* bits (never cleared by the library) */
+} ippd_batch_t;
+
+/*
+ * KV cache (device buffers of the batch dtype).  Keys are stored rotated at
+ * their virtual positions, token-major; values are stored transposed
+ * (dimension-major, tokens contiguous) so that both operands of the two
+ * products stream with 16-byte loads.
+ *   ctx_k  [Hkv][ctx_pool_tokens][D]      ctx_vt [Hkv][D][ctx_pool_tokens]
+ *   seg_k  [Nt][Hkv][seg_capacity][D]     seg_vt [Nt][Hkv][D][seg_capacity]
+ * All four must be 16-byte aligned.
+ */
+typedef struct ippd_kv_cache {
+  void *ctx_k;
+  void *ctx_vt;
+  void *seg_k;
+  void *seg_vt;
+} ippd_kv_cache_t;
+
+/*
+ * Fill the context part of the cache from raw (pre-rotation) keys and values
+ * k_raw/v_raw [ctx_pool_tokens][Hkv][D], laid out like the pool: token t of
+ * prompt b is row ctx_off[b] + t and is rotated at position t (Sec. 4.1:
+ * context tokens sit at [|p|, |p| + |c_j|), with p folded into the context).
+ * Rows outside every prompt's range are neither read nor written.
+ * Stands in for the prefill that would produce this cache.
+ */
+ippd_status_t ippd_load_context(const ippd_batch_t *batch, const void *k_raw,
+                                const void *v_raw, const ippd_kv_cache_t *kv,
+                                hipStream_t stream);
+
+/*
+ * Fill segments from raw keys/values k_raw/v_raw [Nt][seg_capacity][Hkv][D]:
+ * slots 0..init_len[i]-1 of question i are rotated at ctx_len[b] + slot
+ * (Sec. 4.1 question/answer positions) and seg_len[i] is set to init_len[i]
+ * (device [Nt], each <= seg_capacity; larger values set IPPD_FLAG_BAD_LAYOUT
+ * and leave the question untouched).
+ */
+ippd_status_t ippd_load_segments(const ippd_batch_t *batch, const void *k_raw,
+                                 const void *v_raw, const int32_t *init_len,
+                                 const ippd_kv_cache_t *kv, hipStream_t stream);
+
+/*
+ * Decode-step rotation and append (Sec. 4.1 virtual position of answer
+ * tokens; Sec. 4.2 "appended with the correct virtual position").
+ * For every active question i of prompt b, with s = seg_len[i] and
+ * pos = ctx_len[b] + s:
+ *   q_rot[i][h] = R(pos) q_new[i][h]        for all Hq heads,
+ *   seg slot s of (i, g) <- (R(pos) k_new[i][g], v_new[i][g]),
+ *   seg_len[i] = s + 1.
+ * q_new [Nt][Hq][D], k_new/v_new [Nt][Hkv][D], q_rot [Nt][Hq][D], all of
+ * the batch dtype.  Inactive questions are untouched (no append, q_rot rows
+ * not written).  s == seg_capacity sets IPPD_FLAG_SEGMENT_FULL and skips i.
+ */
+ippd_status_t ippd_append_kv(const ippd_batch_t *batch, const void *q_new,
+                             const void *k_new, const void *v_new, void *q_rot,
+                             const ippd_kv_cache_t *kv, hipStream_t stream);
+
+/* Workspace bytes needed by ippd_decode_attention / standard_decode_attention
+ * for this batch (depends only on host-side fields).  Returns 0 for an
+ * invalid batch. */
+size_t ippd_decode_workspace_bytes(const ippd_batch_t *batch);
+size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
+
+/*
+ * IPPD decode-step attention (Sec. 4.1 mask, Sec. 4.2 attn_IPPD).  For every
+ * active question i (prompt b) and query head h (kv head g):
+ *   out[i][h] = softmax_k( scale * q_rot[i][h] . K_k ) V_k
+ * over the keys of prompt b's context and of segment (i, g) slots
+ * 0..seg_len[i]-1 (call after ippd_append_kv, so the step's own token is the
+ * last key).  Each context tile is read from HBM once for ALL active
+ * questions and all heads of its kv group; the context is split into chunks
+ * whose partial softmax states (max, sum, weighted values) are merged
+ * exactly.  lse[i][h] = natural-log sum of exp over the same logits
+ * (optional, may be NULL).  out [Nt][Hq][D] and lse [Nt][Hq] are float32;
+ * rows of inactive questions are not written.
+ * workspace: device scratch of >= ippd_decode_workspace_bytes(batch) bytes,
+ * 256-byte aligned, exclusive to this call until it completes.
+ */
+ippd_status_t ippd_decode_attention(const ippd_batch_t *batch, const void *q_rot,
+                                    const ippd_kv_cache_t *kv, float *out, float *lse,
+                                    void *workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/*
+ * Baseline: the same result computed as standard decoding does it (Sec. 3,
+ * batched autoregressive inference; App. A.2.2 PC+PA decode, one query per
+ * attention over |p|+|c_j|+|x|+|y_<t| keys): every question attends to its
+ * prompt's context separately, so the context is re-read once per active
+ * question.  Same arguments and semantics as ippd_decode_attention;
+ * workspace >= standard_decode_workspace_bytes(batch).
+ */
+ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q_rot,
+                                        const ippd_kv_cache_t *kv, float *out, float *lse,
+                                        void *workspace, size_t workspace_bytes,
+                                        hipStream_t stream);
+
+/* Static description of a status code. */
+const char *ippd_status_string(ippd_status_t status);
+
+/* hipError_t of the most recent IPPD_ERR_HIP on the calling thread (0 if none). */
+int ippd_last_hip_error(void);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int ippd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IPPD_H */

@@ -1,0 +1,206 @@
+// Rotary embedding at virtual positions, KV append, and cache loaders.
+//
+// Positions follow the virtual-position rule of Sec. 4.1: a context token t
+// sits at t (instruction folded into the context), segment slot t of a
+// question of prompt b at ctx_len[b] + t, and the token fed at a decode step
+// at ctx_len[b] + seg_len[i].  Angles pos * theta_j are formed in fp64 (a
+// fp32 product loses ~pos * 6e-8 rad), rotated values are rounded once to
+// the cache dtype.
+#include "ippd_device.h"
+#include "ippd_internal.h"
+
+namespace ippd {
+
+// cos/sin(pos * theta_j) for j < D/2 into LDS, theta_j = base^(-2j/D).
+__device__ __forceinline__ void rope_table(double* s_cos, double* s_sin, int D, double base,
+                                           int64_t pos) {
+  for (int j = threadIdx.x; j < D / 2; j += blockDim.x) {
+    double theta = pow(base, -2.0 * j / D);
+    double ang = static_cast<double>(pos) * theta;
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    s_cos[j] = cs;
+    s_sin[j] = sn;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void rotate_pair(const T* src, T* dst, int j, int half,
+                                            double cs, double sn) {
+  double x = to_f32<T>(src[j]);
+  double y = to_f32<T>(src[j + half]);
+  dst[j] = from_f32<T>(static_cast<float>(x * cs - y * sn));
+  dst[j + half] = from_f32<T>(static_cast<float>(y * cs + x * sn));
+}
+
+// ---------------------------------------------------------------------------
+// Decode-step append: one workgroup per question.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
+  __shared__ double s_cos[64], s_sin[64];
+  const int i = blockIdx.x;
+  if (i >= p.Nt || !p.active[i]) return;
+  const int b = prompt_of(p.q_start, p.B, i);
+  const int s = p.seg_len[i];
+  if (s < 0 || s >= p.seg_cap) {
+    if (threadIdx.x == 0) raise_flag(p.err_flag, s >= p.seg_cap ? kFlagSegmentFull : kFlagBadLayout);
+    return;
+  }
+  const int D = p.D, half = D / 2;
+  const int64_t pos = static_cast<int64_t>(p.ctx_len[b]) + s;
+  rope_table(s_cos, s_sin, D, p.base, pos);
+  __syncthreads();
+
+  const T* qn = static_cast<const T*>(p.q_new);
+  const T* kn = static_cast<const T*>(p.k_new);
+  const T* vn = static_cast<const T*>(p.v_new);
+  T* qr = static_cast<T*>(p.q_rot);
+  T* sk = static_cast<T*>(p.seg_k);
+  T* svt = static_cast<T*>(p.seg_vt);
+  const int heads = p.Hq + p.Hkv;
+  for (int e = threadIdx.x; e < heads * half; e += blockDim.x) {
+    const int hh = e / half, j = e - hh * half;
+    if (hh < p.Hq) {
+      const int64_t off = (static_cast<int64_t>(i) * p.Hq + hh) * D;
+      rotate_pair<T>(qn + off, qr + off, j, half, s_cos[j], s_sin[j]);
+    } else {
+      const int g = hh - p.Hq;
+      const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D;
+      const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * p.seg_cap + s) * D;
+      rotate_pair<T>(kn + src, sk + dst, j, half, s_cos[j], s_sin[j]);
+    }
+  }
+  for (int e = threadIdx.x; e < p.Hkv * D; e += blockDim.x) {
+    const int g = e / D, d = e - g * D;
+    const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D + d;
+    const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * D + d) * p.seg_cap + s;
+    svt[dst] = vn[src];
+  }
+  __syncthreads();   // every thread has read seg_len[i] before it moves
+  if (threadIdx.x == 0) p.seg_len[i] = s + 1;
+}
+
+// ---------------------------------------------------------------------------
+// Context loader: workgroup per (prompt b, 64-token tile, kv head g).
+// ---------------------------------------------------------------------------
+constexpr int kLoadTile = 64;
+
+template <typename T>
+__global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, int tiles_per_prompt) {
+  __shared__ T s_v[kLoadTile][128 + 1];
+  const int g = blockIdx.y;
+  const int b = blockIdx.x / tiles_per_prompt;
+  const int tile = blockIdx.x - b * tiles_per_prompt;
+  const int64_t off = p.ctx_off[b];
+  const int len = p.ctx_len[b];
+  if (off < 0 || (off & 7) || len < 0 || len > p.max_ctx_len || off + len > p.pool) {
+    if (threadIdx.x == 0 && tile == 0 && g == 0) raise_flag(p.err_flag, kFlagBadLayout);
+    return;
+  }
+  const int t0 = tile * kLoadTile;
+  if (t0 >= len) return;
+  const int nt = min(kLoadTile, len - t0);
+  const int D = p.D, half = D / 2;
+  const T* kr = static_cast<const T*>(p.k_raw);
+  const T* vr = static_cast<const T*>(p.v_raw);
+  T* ck = static_cast<T*>(p.ctx_k);
+  T* cvt = static_cast<T*>(p.ctx_vt);
+  // keys: rotate at position t (pair per thread; fp64 angle per pair)
+  for (int e = threadIdx.x; e < nt * half; e += blockDim.x) {
+    const int tt = e / half, j = e - tt * half;
+    const int t = t0 + tt;
+    const double theta = pow(p.base, -2.0 * j / D);
+    double sn, cs;
+    sincos(static_cast<double>(t) * theta, &sn, &cs);
+    const int64_t src = ((off + t) * p.Hkv + g) * D;
+    const int64_t dst = (static_cast<int64_t>(g) * p.pool + off + t) * D;
+    rotate_pair<T>(kr + src, ck + dst, j, half, cs, sn);
+  }
+  // values: transpose a [tokens][D] tile into [D][tokens] through LDS
+  for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
+    const int tt = e / D, d = e - tt * D;
+    s_v[tt][d] = vr[((off + t0 + tt) * p.Hkv + g) * D + d];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
+    const int d = e / nt, tt = e - d * nt;
+    cvt[(static_cast<int64_t>(g) * D + d) * p.pool + off + t0 + tt] = s_v[tt][d];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segment loader: workgroup per (question i, 64-slot tile, kv head g).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void load_segments_kernel(LoadSegmentsParams p, int tiles) {
+  __shared__ T s_v[kLoadTile][128 + 1];
+  const int g = blockIdx.y;
+  const int i = blockIdx.x / tiles;
+  const int tile = blockIdx.x - i * tiles;
+  const int n = p.init_len[i];
+  if (n < 0 || n > p.seg_cap) {
+    if (threadIdx.x == 0 && tile == 0 && g == 0) raise_flag(p.err_flag, kFlagBadLayout);
+    return;
+  }
+  const int b = prompt_of(p.q_start, p.B, i);
+  if (threadIdx.x == 0 && tile == 0 && g == 0) p.seg_len[i] = n;
+  const int t0 = tile * kLoadTile;
+  if (t0 >= n) return;
+  const int nt = min(kLoadTile, n - t0);
+  const int D = p.D, half = D / 2;
+  const int64_t base_pos = p.ctx_len[b];
+  const T* kr = static_cast<const T*>(p.k_raw);
+  const T* vr = static_cast<const T*>(p.v_raw);
+  T* sk = static_cast<T*>(p.seg_k);
+  T* svt = static_cast<T*>(p.seg_vt);
+  for (int e = threadIdx.x; e < nt * half; e += blockDim.x) {
+    const int tt = e / half, j = e - tt * half;
+    const int t = t0 + tt;
+    const double theta = pow(p.base, -2.0 * j / D);
+    double sn, cs;
+    sincos(static_cast<double>(base_pos + t) * theta, &sn, &cs);
+    const int64_t src = ((static_cast<int64_t>(i) * p.seg_cap + t) * p.Hkv + g) * D;
+    const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * p.seg_cap + t) * D;
+    rotate_pair<T>(kr + src, sk + dst, j, half, cs, sn);
+  }
+  for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
+    const int tt = e / D, d = e - tt * D;
+    s_v[tt][d] = vr[((static_cast<int64_t>(i) * p.seg_cap + t0 + tt) * p.Hkv + g) * D + d];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
+    const int d = e / nt, tt = e - d * nt;
+    svt[((static_cast<int64_t>(i) * p.Hkv + g) * D + d) * p.seg_cap + t0 + tt] = s_v[tt][d];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers.
+// ---------------------------------------------------------------------------
+hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s) {
+  const int tiles = (p.max_ctx_len + kLoadTile - 1) / kLoadTile;
+  if (tiles == 0 || p.B == 0) return hipSuccess;
+  dim3 grid(static_cast<unsigned>(p.B) * tiles, p.Hkv);
+  if (dtype == 0) load_context_kernel<float><<<grid, 256, 0, s>>>(p, tiles);
+  else load_context_kernel<uint16_t><<<grid, 256, 0, s>>>(p, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s) {
+  const int tiles = (p.seg_cap + kLoadTile - 1) / kLoadTile;
+  if (p.Nt == 0) return hipSuccess;
+  dim3 grid(static_cast<unsigned>(p.Nt) * tiles, p.Hkv);
+  if (dtype == 0) load_segments_kernel<float><<<grid, 256, 0, s>>>(p, tiles);
+  else load_segments_kernel<uint16_t><<<grid, 256, 0, s>>>(p, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s) {
+  if (p.Nt == 0) return hipSuccess;
+  if (dtype == 0) append_kernel<float><<<p.Nt, 256, 0, s>>>(p);
+  else append_kernel<uint16_t><<<p.Nt, 256, 0, s>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace ippd

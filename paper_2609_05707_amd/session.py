@@ -1,0 +1,179 @@
+"""Torch-side buffers for one batch of stacked prompts, wired to the C ABI.
+
+PyTorch only provides device memory and the stream here.  A DecodeBatch
+owns, per emulated layer, the KV cache of the library layout and the
+segment-length counters; it fills ``ippd_batch_t`` / ``ippd_kv_cache_t``
+structs and forwards every operation to libippd.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+
+def _round8(x: int) -> int:
+    return (int(x) + 7) // 8 * 8
+
+
+def torch_dtype(dtype: str):
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+class DecodeBatch:
+    """B prompts (context lengths ``ctx_len``, question counts ``q_count``) on one GPU.
+
+    Context pool: prompt b at token offset ctx_off[b] (multiples of 8, packed).
+    ``layers`` independent caches share the structure arrays and the active
+    mask; each layer has its own seg_len counters (advanced by its appends).
+    """
+
+    def __init__(self, ctx_len: Sequence[int], q_count: Sequence[int], hq: int, hkv: int,
+                 head_dim: int, dtype: str, seg_capacity: int, rope_base: float = 10000.0,
+                 scale: float = 0.0, chunk_tokens: int = 0, max_questions: Optional[int] = None,
+                 layers: int = 1, device: str = "cuda"):
+        self.device = torch.device(device)
+        self.dtype = dtype
+        self.tdtype = torch_dtype(dtype)
+        self.B = len(ctx_len)
+        self.ctx_len = np.asarray(ctx_len, dtype=np.int64)
+        self.q_count = np.asarray(q_count, dtype=np.int64)
+        self.Nt = int(self.q_count.sum())
+        self.hq, self.hkv, self.D = hq, hkv, head_dim
+        self.seg_cap = _round8(max(seg_capacity, 8))
+        self.layers = layers
+        padded = np.array([_round8(x) for x in self.ctx_len], dtype=np.int64)
+        self.ctx_off = np.concatenate([[0], np.cumsum(padded)[:-1]]).astype(np.int64)
+        self.pool = max(8, int(padded.sum()))
+        self.q_start = np.concatenate([[0], np.cumsum(self.q_count)]).astype(np.int32)
+        self.max_ctx_len = int(self.ctx_len.max()) if self.B else 0
+        self.max_questions = int(max_questions if max_questions is not None
+                                 else max(1, int(self.q_count.max())))
+        dev = self.device
+        self.d_ctx_off = torch.from_numpy(self.ctx_off).to(dev)
+        self.d_ctx_len = torch.from_numpy(self.ctx_len.astype(np.int32)).to(dev)
+        self.d_q_start = torch.from_numpy(self.q_start).to(dev)
+        self.d_active = torch.ones(max(self.Nt, 1), dtype=torch.uint8, device=dev)
+        self.d_err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.seg_len = [torch.zeros(max(self.Nt, 1), dtype=torch.int32, device=dev) for _ in range(layers)]
+        td = self.tdtype
+        self.ctx_k = [torch.empty(hkv, self.pool, head_dim, dtype=td, device=dev) for _ in range(layers)]
+        self.ctx_vt = [torch.empty(hkv, head_dim, self.pool, dtype=td, device=dev) for _ in range(layers)]
+        nt = max(self.Nt, 1)
+        self.seg_k = [torch.empty(nt, hkv, self.seg_cap, head_dim, dtype=td, device=dev) for _ in range(layers)]
+        self.seg_vt = [torch.empty(nt, hkv, head_dim, self.seg_cap, dtype=td, device=dev) for _ in range(layers)]
+        self.batches = []
+        self.caches = []
+        for layer in range(layers):
+            bt = L.IppdBatch()
+            bt.num_prompts = self.B
+            bt.num_questions = self.Nt
+            bt.num_q_heads = hq
+            bt.num_kv_heads = hkv
+            bt.head_dim = head_dim
+            bt.dtype = L.IPPD_DTYPE_F32 if dtype == "f32" else L.IPPD_DTYPE_BF16
+            bt.ctx_pool_tokens = self.pool
+            bt.seg_capacity = self.seg_cap
+            bt.max_ctx_len = self.max_ctx_len
+            bt.max_questions = self.max_questions
+            bt.chunk_tokens = chunk_tokens
+            bt.rope_base = rope_base
+            bt.scale = scale
+            bt.ctx_off = self.d_ctx_off.data_ptr()
+            bt.ctx_len = self.d_ctx_len.data_ptr()
+            bt.q_start = self.d_q_start.data_ptr()
+            bt.seg_len = self.seg_len[layer].data_ptr()
+            bt.active = self.d_active.data_ptr()
+            bt.err_flag = self.d_err.data_ptr()
+            self.batches.append(bt)
+            kv = L.IppdKvCache()
+            kv.ctx_k = self.ctx_k[layer].data_ptr()
+            kv.ctx_vt = self.ctx_vt[layer].data_ptr()
+            kv.seg_k = self.seg_k[layer].data_ptr()
+            kv.seg_vt = self.seg_vt[layer].data_ptr()
+            self.caches.append(kv)
+        self.ws_ippd_bytes = L.ippd_decode_workspace_bytes(self.batches[0])
+        self.ws_std_bytes = L.standard_decode_workspace_bytes(self.batches[0])
+        self.ws_ippd = torch.empty(max(self.ws_ippd_bytes, 256), dtype=torch.uint8, device=dev)
+        self.ws_std = torch.empty(max(self.ws_std_bytes, 256), dtype=torch.uint8, device=dev)
+        self.q_rot = torch.empty(nt, hq, head_dim, dtype=td, device=dev)
+        self.out = torch.empty(nt, hq, head_dim, dtype=torch.float32, device=dev)
+        self.lse = torch.empty(nt, hq, dtype=torch.float32, device=dev)
+
+    # ------------------------------------------------------------------ helpers
+    @staticmethod
+    def stream() -> int:
+        return torch.cuda.current_stream().cuda_stream
+
+    def to_dev(self, x) -> torch.Tensor:
+        t = x if isinstance(x, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(x))
+        return t.to(self.device).to(self.tdtype).contiguous()
+
+    def err_flag(self) -> int:
+        return int(self.d_err.item())
+
+    # ------------------------------------------------------------------ loading
+    def load_context(self, layer: int, k_packed, v_packed) -> None:
+        """k/v_packed: [sum ctx_len, Hkv, D] raw (pre-rotation), prompts in order."""
+        kp, vp = self.to_dev(k_packed), self.to_dev(v_packed)
+        k_raw = torch.zeros(self.pool, self.hkv, self.D, dtype=self.tdtype, device=self.device)
+        v_raw = torch.zeros_like(k_raw)
+        src = 0
+        for b in range(self.B):
+            n = int(self.ctx_len[b])
+            o = int(self.ctx_off[b])
+            k_raw[o:o + n] = kp[src:src + n]
+            v_raw[o:o + n] = vp[src:src + n]
+            src += n
+        L.ippd_load_context(self.batches[layer], k_raw.data_ptr(), v_raw.data_ptr(),
+                            self.caches[layer], self.stream())
+        torch.cuda.current_stream().synchronize()
+
+    def load_segments(self, layer: int, k_packed, v_packed, seg_len0) -> None:
+        """k/v_packed: [sum seg_len0, Hkv, D] raw; question i owns the next seg_len0[i] rows."""
+        seg_len0 = np.asarray(seg_len0, dtype=np.int64)
+        if self.Nt and int(seg_len0.max()) > self.seg_cap:
+            raise ValueError("initial segment longer than seg_capacity")
+        kp, vp = self.to_dev(k_packed), self.to_dev(v_packed)
+        nt = max(self.Nt, 1)
+        k_raw = torch.zeros(nt, self.seg_cap, self.hkv, self.D, dtype=self.tdtype, device=self.device)
+        v_raw = torch.zeros_like(k_raw)
+        starts = np.concatenate([[0], np.cumsum(seg_len0)])
+        for i in range(self.Nt):
+            n = int(seg_len0[i])
+            k_raw[i, :n] = kp[starts[i]:starts[i] + n]
+            v_raw[i, :n] = vp[starts[i]:starts[i] + n]
+        init = torch.from_numpy(seg_len0.astype(np.int32)).to(self.device)
+        L.ippd_load_segments(self.batches[layer], k_raw.data_ptr(), v_raw.data_ptr(), init.data_ptr(),
+                             self.caches[layer], self.stream())
+        torch.cuda.current_stream().synchronize()
+
+    def set_active(self, mask) -> None:
+        m = torch.as_tensor(np.asarray(mask, dtype=np.uint8))
+        self.d_active[: self.Nt].copy_(m.to(self.device))
+
+    # ------------------------------------------------------------------ hot path
+    def append(self, layer: int, q_new: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+               q_rot: Optional[torch.Tensor] = None) -> None:
+        q_rot = self.q_rot if q_rot is None else q_rot
+        L.ippd_append_kv(self.batches[layer], q_new.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+                         q_rot.data_ptr(), self.caches[layer], self.stream())
+
+    def decode(self, layer: int, standard: bool = False, q_rot: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+               with_lse: bool = True) -> None:
+        q_rot = self.q_rot if q_rot is None else q_rot
+        out = self.out if out is None else out
+        lse = self.lse if lse is None else lse
+        lse_ptr = lse.data_ptr() if with_lse else None
+        if standard:
+            L.standard_decode_attention(self.batches[layer], q_rot.data_ptr(), self.caches[layer],
+                                        out.data_ptr(), lse_ptr, self.ws_std.data_ptr(),
+                                        self.ws_std_bytes, self.stream())
+        else:
+            L.ippd_decode_attention(self.batches[layer], q_rot.data_ptr(), self.caches[layer],
+                                    out.data_ptr(), lse_ptr, self.ws_ippd.data_ptr(),
+                                    self.ws_ippd_bytes, self.stream())

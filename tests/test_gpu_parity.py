@@ -1,0 +1,269 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Tolerances: max |gpu - oracle| <= 1e-5 for fp32 workloads, <= 2e-2 for bf16
+operands with fp32 accumulation, on out and on lse.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workload as W
+from oracle import ippd as O
+from tests.gpu_harness import (load_layer, log, make_batch, max_err, oracle_steps, run_gpu)
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def check(st, gpu, ref, steps, label, qsel=None):
+    tol = TOL[st.wl.dtype]
+    for t in steps:
+        ro, rl = ref[t]
+        go, gl = gpu.out[t], gpu.lse[t]
+        if qsel is not None:
+            idx = [i for i in qsel[t] if st.active(t)[i]]
+            ro, rl, go, gl = ro[idx], rl[idx], go[idx], gl[idx]
+        eo, el = max_err(go, ro), max_err(gl, rl)
+        log(f"{label} step {t}: max|out err| {eo:.3e}  max|lse err| {el:.3e}  (tol {tol})")
+        assert eo <= tol and el <= tol, (label, t, eo, el)
+
+
+# ------------------------------------------------------------------ tiny fp32
+
+def test_tiny_f32_full():
+    log("case: tiny fp32 workload, 1 step")
+    wl = W.workload(1)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0], [0], kv=kv)
+    ref = oracle_steps(st, kv, [0], [0])
+    assert gpu.err == 0
+    check(st, gpu, ref, [0], "tiny-f32")
+
+    # rotated query and the appended key/value at virtual position Lc + s_i
+    si = W.step_inputs(st, 0)
+    pos = st.ctx_len[0] + st.seg_len0
+    q_ref = O.rope(si.q_new, pos[:, None], wl.rope_base)
+    np.testing.assert_allclose(gpu.q_rot[0], q_ref, atol=2e-6, rtol=0)
+    db = gpu.batch
+    seg_k = db.seg_k[0].float().cpu().numpy()
+    seg_vt = db.seg_vt[0].float().cpu().numpy()
+    for i in range(st.num_questions):
+        s = st.seg_len0[i]
+        k_ref = O.rope(si.k_new[i], pos[i], wl.rope_base)
+        np.testing.assert_allclose(seg_k[i, :, s], k_ref, atol=2e-6, rtol=0)
+        np.testing.assert_array_equal(seg_vt[i, :, :, s], si.v_new[i])
+    assert db.seg_len[0][: st.num_questions].cpu().numpy().tolist() == (st.seg_len0 + 1).tolist()
+    # context cache rotated at positions 0..Lc-1, values transposed
+    ck = db.ctx_k[0].float().cpu().numpy()
+    k_ctx_ref = O.rope(kv.ctx_k.transpose(1, 0, 2), np.arange(256)[None, :], wl.rope_base)
+    np.testing.assert_allclose(ck[:, :256], k_ctx_ref, atol=2e-6, rtol=0)
+    np.testing.assert_array_equal(db.ctx_vt[0].float().cpu().numpy()[:, :, :256],
+                                  kv.ctx_v.transpose(1, 2, 0))
+
+
+# ------------------------------------------------------------- small ragged
+
+def ragged_workload(dtype, d=64, hq=8, hkv=2, steps=3, seed_id=200):
+    return W.custom_workload(wid=seed_id, dtype=dtype, num_prompts=3, hq=hq, hkv=hkv, head_dim=d,
+                             ctx_len=(40, 200), questions=(1, 6), question_tokens=0,
+                             seg_len=(1, 40), steps=steps, stop=(1, steps),
+                             value_std=1.0 if dtype == "f32" else 0.5)
+
+
+@pytest.mark.parametrize("dtype,d,chunk", [("f32", 64, 0), ("f32", 128, 32), ("bf16", 128, 0),
+                                           ("bf16", 128, 64), ("bf16", 64, 32)])
+def test_small_ragged(dtype, d, chunk):
+    log(f"case: small ragged dtype={dtype} D={d} chunk={chunk}")
+    st = W.make_structure(ragged_workload(dtype, d))
+    kv = W.layer_kv(st)
+    steps = list(range(st.wl.steps))
+    gpu = run_gpu(st, steps, steps, chunk_tokens=chunk, kv=kv)
+    ref = oracle_steps(st, kv, steps, steps)
+    assert gpu.err == 0
+    check(st, gpu, ref, steps, f"ragged-{dtype}-{d}-{chunk}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_standard_baseline_matches_oracle(dtype):
+    log(f"case: standard baseline dtype={dtype}")
+    st = W.make_structure(ragged_workload(dtype, 128))
+    kv = W.layer_kv(st)
+    steps = list(range(st.wl.steps))
+    gpu = run_gpu(st, steps, steps, standard=True, kv=kv)
+    ref = oracle_steps(st, kv, steps, steps)
+    check(st, gpu, ref, steps, f"standard-{dtype}")
+
+
+def test_inactive_rows_untouched_and_not_appended():
+    log("case: inactive rows keep the sentinel, their segments do not grow")
+    st = W.make_structure(ragged_workload("bf16", 128, steps=4))
+    kv = W.layer_kv(st)
+    steps = list(range(4))
+    gpu = run_gpu(st, steps, steps, sentinel=-777.0, kv=kv)
+    for t in steps:
+        dead = ~st.active(t)
+        assert np.all(gpu.out[t][dead] == -777.0) and np.all(gpu.lse[t][dead] == -777.0)
+        assert not np.any(gpu.out[t][~dead] == -777.0)
+    got = gpu.batch.seg_len[0][: st.num_questions].cpu().numpy()
+    np.testing.assert_array_equal(got, st.seg_len_at(4))
+
+
+def test_split_count_and_batch_independence():
+    """Chunking regroups exact sums (results agree across chunk sizes); a prompt's
+    output does not depend on the other prompts of the batch (Sec. 4.4)."""
+    log("case: split-count / batch independence")
+    wl = W.custom_workload(wid=210, dtype="bf16", num_prompts=3, hq=32, hkv=8, head_dim=128,
+                           ctx_len=(300, 900), questions=(3, 9), seg_len=(5, 60), steps=1)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    outs = {}
+    for ch in (32, 96, 256, 1024):
+        outs[ch] = run_gpu(st, [0], [0], chunk_tokens=ch, kv=kv).out[0]
+    ref = oracle_steps(st, kv, [0], [0])
+    for ch, o in outs.items():
+        e = max_err(o, ref[0][0])
+        log(f"chunk {ch}: max err {e:.3e}")
+        assert e <= TOL["bf16"]
+        assert np.max(np.abs(o - outs[32])) <= 2e-3
+    # prompt 1 alone
+    b = 1
+    st1 = W.Structure(wl, st.ctx_len[b:b + 1], st.q_count[b:b + 1],
+                      st.seg_len0[st.q_start[b]:st.q_start[b + 1]], st.stop[st.q_start[b]:st.q_start[b + 1]])
+    kv1 = W.LayerKV(kv.ctx_k[st.ctx_start[b]:st.ctx_start[b + 1]], kv.ctx_v[st.ctx_start[b]:st.ctx_start[b + 1]],
+                    kv.seg_k[st.seg_start[st.q_start[b]]:st.seg_start[st.q_start[b + 1]]],
+                    kv.seg_v[st.seg_start[st.q_start[b]]:st.seg_start[st.q_start[b + 1]]])
+    db = make_batch(st1, chunk_tokens=96, max_questions=int(st.q_count.max()))
+    load_layer(db, st1, 0, kv1)
+    si = W.step_inputs(st, 0)
+    sl = slice(st.q_start[b], st.q_start[b + 1])
+    db.set_active(si.active[sl])
+    db.append(0, db.to_dev(si.q_new[sl]), db.to_dev(si.k_new[sl]), db.to_dev(si.v_new[sl]))
+    db.decode(0)
+    alone = db.out[: st1.num_questions].cpu().numpy()
+    np.testing.assert_array_equal(alone, outs[96][sl])
+
+
+def test_empty_context_and_many_questions():
+    log("case: a prompt with an empty context and a prompt with 300 questions")
+    wl = W.custom_workload(wid=220, dtype="bf16", num_prompts=2, hq=8, hkv=2, head_dim=128,
+                           steps=1)
+    rng = np.random.default_rng(5)
+    q_count = np.array([3, 300])
+    st = W.Structure(wl, np.array([0, 150]), q_count, rng.integers(1, 20, size=303),
+                     np.full(303, 1))
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0], [0], kv=kv)
+    assert gpu.err == 0
+    sel = {0: list(range(0, 303, 7)) + [0, 1, 2]}
+    ref = oracle_steps(st, kv, [0], [0], questions=sel)
+    check(st, gpu, ref, [0], "empty-ctx/300q", qsel=sel)
+
+
+def test_rope_base_500000_f32():
+    log("case: rope base 5e5, fp32")
+    wl = W.custom_workload(wid=230, dtype="f32", num_prompts=2, hq=4, hkv=4, head_dim=64,
+                           ctx_len=(500, 700), questions=(2, 3), seg_len=(3, 9), steps=2,
+                           rope_base=500000.0, value_std=1.0)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0, 1], [0, 1], kv=kv)
+    ref = oracle_steps(st, kv, [0, 1], [0, 1])
+    check(st, gpu, ref, [0, 1], "base5e5")
+
+
+def test_all_inactive_step_is_a_noop():
+    log("case: every question stopped")
+    st = W.make_structure(ragged_workload("bf16", 128, steps=2))
+    db = make_batch(st)
+    load_layer(db, st, 0, W.layer_kv(st))
+    si = W.step_inputs(st, 0)
+    db.set_active(np.zeros(st.num_questions, bool))
+    db.out.fill_(3.0)
+    before = db.seg_len[0].clone()
+    db.append(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new))
+    db.decode(0)
+    torch.cuda.synchronize()
+    assert torch.all(db.out == 3.0)
+    assert torch.equal(db.seg_len[0], before)
+    assert db.err_flag() == 0
+
+
+def test_device_side_flags():
+    log("case: segment overflow and bad layout raise flags, nothing else")
+    st = W.make_structure(ragged_workload("bf16", 64, steps=1))
+    db = make_batch(st, extra_cap=0)
+    load_layer(db, st, 0, W.layer_kv(st))
+    # fill every segment to capacity, then append: overflow flag, seg_len unchanged
+    db.seg_len[0][: st.num_questions] = db.seg_cap
+    si = W.step_inputs(st, 0)
+    db.set_active(np.ones(st.num_questions, bool))
+    db.append(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new))
+    torch.cuda.synchronize()
+    assert db.err_flag() & 1
+    assert int(db.seg_len[0][0]) == db.seg_cap
+    # misaligned context offset: attention skips the prompt and flags it
+    db.d_err.zero_()
+    db.d_ctx_off[0] = 3
+    db.decode(0)
+    torch.cuda.synchronize()
+    assert db.err_flag() & 2
+
+
+# -------------------------------------------------------- full-size workloads
+
+def test_llama3_8b_lc4096_n16_64_steps():
+    log("case: workload 2 (Lc 4096, N 16, 64 steps), sampled steps vs oracle")
+    st = W.make_structure(W.workload(2))
+    kv = W.layer_kv(st)
+    steps = list(range(64))
+    rec = [0, 1, 32, 63]
+    gpu = run_gpu(st, steps, rec, kv=kv)
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, steps, rec)
+    check(st, gpu, ref, rec, "wl2")
+    std = run_gpu(st, [0], [0], standard=True, kv=kv)
+    check(st, std, {0: ref[0]}, [0], "wl2-standard")
+
+
+def test_ragged_b32_sampled():
+    log("case: workload 3 (B 32 ragged, 32 steps), sampled questions vs oracle")
+    st = W.make_structure(W.workload(3))
+    kv = W.layer_kv(st)
+    steps = list(range(32))
+    rec = [0, 31]
+    rng = np.random.default_rng(0)
+    sel = {t: sorted(rng.choice(st.num_questions, 20, replace=False).tolist()) for t in rec}
+    gpu = run_gpu(st, steps, rec, kv=kv)
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, steps, rec, questions=sel)
+    check(st, gpu, ref, rec, "wl3", qsel=sel)
+
+
+def test_long_context_sampled():
+    log("case: workload 4 (Lc 32768, N 64, 32 steps), sampled questions vs oracle")
+    st = W.make_structure(W.workload(4))
+    kv = W.layer_kv(st)
+    steps = list(range(32))
+    rec = [0, 31]
+    sel = {0: [0, 17, 40, 63], 31: [5, 33, 62]}
+    gpu = run_gpu(st, steps, rec, kv=kv)
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, steps, rec, questions=sel)
+    check(st, gpu, ref, rec, "wl4", qsel=sel)
+
+
+@pytest.mark.parametrize("layer", [0, 31])
+def test_32layer_sampled(layer):
+    log(f"case: workload 5 layer {layer} (B 8, Lc 8192, 128 steps, shrinking active set)")
+    st = W.make_structure(W.workload(5))
+    kv = W.layer_kv(st, layer)
+    steps = list(range(128))
+    rec = [0, 15, 64, 127]
+    rng = np.random.default_rng(layer)
+    sel = {t: sorted(rng.choice(st.num_questions, 8, replace=False).tolist()) for t in rec}
+    gpu = run_gpu(st, steps, rec, layer=layer, kv=kv)
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, steps, rec, layer=layer, questions=sel)
+    check(st, gpu, ref, rec, f"wl5-L{layer}", qsel=sel)
