@@ -1,0 +1,315 @@
+#!/usr/bin/env python3
+"""Benchmark of the IPPD decode-step hot path on one MI355X.
+
+A step is one decode step of the workload: for every emulated layer, one
+ippd_decode_step launch (virtual-position rotation + KV append, shared-context
+and own-segment attention, exact merge), queued back-to-back on one stream
+with all inputs resident in HBM.  Each layer has
+its own KV cache (same values, distinct buffers), so a step streams every
+layer's context from HBM rather than from the 256 MB Infinity Cache.
+
+value = effective decode tokens/s = sum over timed steps and layers of the
+active questions, divided by the wall time of the timed steps (a
+layer-level figure: each layer-step decodes one token per active question
+at that layer).  The same steps are then re-run with the standard baseline
+(standard_decode_step, the context re-read once per question) on
+identical KV, and the fp64 oracle is timed on a bounded sample on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workload as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+METRIC = "effective decode tokens/s (questions×steps/s) + HBM GB/s % of peak, 1 MI355X"
+
+DEFAULT_LAYERS = {1: 1, 2: 32, 3: 1, 4: 4, 5: 32}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed decode steps (default: the workload's)")
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", type=int, default=2, help="workload id (1..5); 2 is the headline")
+    ap.add_argument("--layers", type=int, default=None, help="emulated layers cycled per step")
+    ap.add_argument("--no-standard", action="store_true", help="skip the standard baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--cpu-sample", type=int, default=48, help="question-steps the oracle computes")
+    ap.add_argument("--chunk", type=int, default=0, help="context tokens per unit (0 = library default)")
+    ap.add_argument("--tile-rows", type=int, default=0, help="rows per context unit (0 = library default)")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------- accounting
+
+def step_bytes(st: W.Structure, t: int, standard: bool = False) -> int:
+    """Algorithmic HBM bytes of one fused layer-step at step t.
+
+    Per prompt with an active question: its context K and V once (IPPD) or once
+    per active question (standard), 2*Lc*Hkv*D*e.  Per active question: its cached
+    segment K and V (2*s*Hkv*D*e), the raw q/k/v of the fed token
+    ((Hq + 2*Hkv)*D*e), the appended key/value (2*Hkv*D*e) and the fp32 output
+    rows (Hq*D*4 + Hq*4 for lse)."""
+    wl = st.wl
+    e = wl.elem_bytes
+    D, hq, hkv = wl.head_dim, wl.hq, wl.hkv
+    act = st.active(t)
+    seg = st.seg_len_at(t)
+    tot = 0
+    for b in range(wl.num_prompts):
+        q0, q1 = st.q_start[b], st.q_start[b + 1]
+        n_act = int(act[q0:q1].sum())
+        if n_act == 0:
+            continue
+        ctx = 2 * int(st.ctx_len[b]) * hkv * D * e
+        tot += ctx * (n_act if standard else 1)
+    ia = np.flatnonzero(act)
+    tot += int(np.sum(2 * seg[ia] * hkv * D * e))
+    tot += len(ia) * ((hq + 2 * hkv) * D * e + 2 * hkv * D * e + hq * D * 4 + hq * 4)
+    return tot
+
+
+def step_flops(st: W.Structure, t: int) -> int:
+    wl = st.wl
+    act = st.active(t)
+    seg = st.seg_len_at(t)
+    tot = 0
+    for i in np.flatnonzero(act):
+        b = st.prompt_of[i]
+        tot += 4 * wl.hq * wl.head_dim * (int(st.ctx_len[b]) + int(seg[i]) + 1)
+    return tot
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("decode_step.hip", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
+        with open(os.path.join(ROOT, "paper_2609_05707_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload_id: int):
+    """HBM traffic per attention launch from the committed rocprofv3 counter summary,
+    only if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_decode_step_wl{workload_id}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ----------------------------------------------------------------- cpu oracle
+
+def cpu_baseline(st: W.Structure, kv: W.LayerKV, n_samples: int):
+    """Time the fp64 oracle on the first question-steps of the workload (layer 0)."""
+    from oracle import ippd as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    state = O.KVState.from_packed(kv.seg_k, kv.seg_v, st.seg_start)
+    done = 0
+    t_total = 0.0
+    steps_used = 0
+    for t in range(st.wl.steps):
+        si = W.step_inputs(st, t)
+        act = np.flatnonzero(si.active)
+        take = act[: max(0, n_samples - done)]
+        if len(take):
+            t0 = time.perf_counter()
+            O.decode_step_standard(kv.ctx_k, kv.ctx_v, st.ctx_start, st.q_start, state,
+                                   si.q_new, si.k_new, si.v_new, si.active, st.wl.rope_base,
+                                   questions=take.tolist())
+            t_total += time.perf_counter() - t0
+            done += len(take)
+            steps_used += 1
+        state.append(si.k_new, si.v_new, si.active)
+        if done >= n_samples:
+            break
+    return {"value": done / t_total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} question-steps of layer 0 (steps 0..{steps_used - 1}, all heads), "
+                      f"{t_total:.1f} s of fp64 numpy",
+            "seconds": round(t_total, 2)}
+
+
+# ----------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the decode-attention "
+              "path is measured on a single MI355X and multi-GPU sharding is not part of this build.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_05707_amd.session import DecodeBatch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = W.workload(args.workload)
+    st = W.make_structure(wl)
+    steps = args.steps if args.steps is not None else wl.steps
+    layers = args.layers if args.layers is not None else DEFAULT_LAYERS[wl.wid]
+    data_steps = wl.steps                      # distinct step inputs; cycled if steps > data_steps
+    cap = int(st.seg_len0.max()) + max(steps, args.warmup, data_steps) + 8
+    db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype,
+                     cap, rope_base=wl.rope_base, layers=layers, chunk_tokens=args.chunk,
+                     tile_rows=args.tile_rows)
+    kv0 = W.layer_kv(st, 0)
+    db.load_context(0, kv0.ctx_k, kv0.ctx_v)
+    db.load_segments(0, kv0.seg_k, kv0.seg_v, st.seg_len0)
+    for l in range(1, layers):
+        db.ctx_k[l].copy_(db.ctx_k[0]); db.ctx_vt[l].copy_(db.ctx_vt[0])
+        db.seg_k[l].copy_(db.seg_k[0]); db.seg_vt[l].copy_(db.seg_vt[0])
+        db.seg_len[l].copy_(db.seg_len[0])
+    seg0 = db.seg_len[0].clone()
+    nt = st.num_questions
+    # per-step inputs resident on the device
+    qs, ks, vs, acts = [], [], [], []
+    for t in range(data_steps):
+        si = W.step_inputs(st, t)
+        qs.append(db.to_dev(si.q_new)); ks.append(db.to_dev(si.k_new)); vs.append(db.to_dev(si.v_new))
+        acts.append(torch.from_numpy(si.active.astype(np.uint8)).to(db.device))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def set_step_active(t):
+        ptr = acts[t % data_steps].data_ptr()
+        for bt in db.batches:
+            bt.active = ptr
+
+    def reset():
+        for l in range(layers):
+            db.seg_len[l].copy_(seg0)
+        torch.cuda.synchronize()
+
+    def run(n_steps, standard=False, events=None, separate=False):
+        for t in range(n_steps):
+            d = t % data_steps
+            set_step_active(d)
+            for l in range(layers):
+                if events is not None:
+                    events[t][l][0].record(stream)
+                if separate:
+                    db.append(l, qs[d], ks[d], vs[d])
+                    db.decode(l, standard=standard)
+                else:
+                    db.decode_step(l, qs[d], ks[d], vs[d], standard=standard, write_q_rot=False)
+                if events is not None:
+                    events[t][l][1].record(stream)
+
+    def timed(standard=False, separate=False):
+        reset()
+        run(args.warmup, standard, separate=separate)
+        reset()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run(steps, standard, separate=separate)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3
+
+    def kernel_time(standard=False):
+        """Average duration of the decode-step launches, from HIP events around each
+        launch on the launching stream, over a second pass of the same timed steps."""
+        reset()
+        run(args.warmup, standard)
+        reset()
+        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(layers)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        run(steps, standard, events=ev)
+        torch.cuda.synchronize()
+        durs = [a.elapsed_time(b) / 1e3 for row in ev for (a, b) in row]
+        return float(np.mean(durs)), durs
+
+    t_ippd = timed(False)
+    err = db.err_flag()
+    tokens = sum(int(st.active(t % data_steps).sum()) for t in range(steps)) * layers
+    value = tokens / t_ippd
+    step_b = [step_bytes(st, t % data_steps) for t in range(steps)]
+    bytes_total = sum(step_b) * layers
+    flops_total = sum(step_flops(st, t % data_steps) for t in range(steps)) * layers
+    k_avg, _ = kernel_time(False)
+    bytes_per_launch = float(np.mean(step_b))
+    achieved = bytes_per_launch / k_avg / 1e9
+    traffic = read_traffic(wl.wid)
+    t_sep = timed(False, separate=True)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_ippd / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded normal K/V/Q, rounded to bf16; no dataset)",
+        "config": {
+            "workload": f"{wl.name}: B={wl.num_prompts}, Hq={wl.hq}, Hkv={wl.hkv}, D={wl.head_dim}, "
+                        f"Lc={wl.ctx_len}, N={wl.questions}, {wl.steps} decode steps",
+            "layers_cycled": layers,
+            "chunk_tokens": args.chunk or "auto",
+            "tile_rows": args.tile_rows or "auto",
+            "step": "per layer: one ippd_decode_step launch (append + attention + merge)",
+            "us_per_layer_step": round(t_ippd / (steps * layers) * 1e6, 3),
+            "separate_calls_us_per_layer_step": round(t_sep / (steps * layers) * 1e6, 3),
+        },
+        "hbm_gbps": round(bytes_total / t_ippd / 1e9, 1),
+        "hbm_frac": round(bytes_total / t_ippd / 1e9 / HBM_PEAK_GBPS, 4),
+        "mfma_tflops": round(flops_total / t_ippd / 1e12, 2),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode_step_kernel (ippd_decode_step)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": int(bytes_per_launch),
+            "avg_launch_us": round(k_avg * 1e6, 3),
+        },
+        "err_flag": err,
+    }
+    if not args.no_standard:
+        t_std = timed(True)
+        std_b = [step_bytes(st, t % data_steps, standard=True) for t in range(steps)]
+        ks_avg, _ = kernel_time(True)
+        result["standard"] = {
+            "value": round(tokens / t_std, 1),
+            "ms_per_step": round(t_std / steps * 1e3, 4),
+            "ippd_speedup": round(t_std / t_ippd, 3),
+            "algorithmic_byte_ratio": round(float(np.mean(std_b)) / bytes_per_launch, 3),
+            "avg_launch_us": round(ks_avg * 1e6, 3),
+            "hbm_gbps_algorithmic": round(float(np.mean(std_b)) / ks_avg / 1e9, 1),
+        }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(st, kv0, args.cpu_sample)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -78,7 +78,7 @@ typedef struct ippd_batch {
   int32_t num_prompts;       /* B >= 1 */
   int32_t num_questions;     /* Nt >= 0, total over prompts */
   int32_t num_q_heads;       /* Hq >= 1 */
-  int32_t num_kv_heads;      /* Hkv >= 1, Hq % Hkv == 0, Hq/Hkv <= 64 */
+  int32_t num_kv_heads;      /* Hkv >= 1, Hq % Hkv == 0, Hq/Hkv <= 16 */
   int32_t head_dim;          /* D: 64 or 128 */
   int32_t dtype;             /* ippd_dtype_t */
   int64_t ctx_pool_tokens;   /* context pool capacity, multiple of 8 */
@@ -87,6 +87,8 @@ typedef struct ippd_batch {
   int32_t max_questions;     /* host bound on questions per prompt, 1..1024 */
   int32_t chunk_tokens;      /* context tokens per work unit: 0 = automatic,
                                 else a multiple of 32 (tests use it to vary splits) */
+  int32_t tile_rows;         /* query rows per context unit: 0 = automatic, else 16, 32,
+                                64 or 128 (a tuning knob; results do not depend on it) */
   double  rope_base;         /* > 0, e.g. 10000 */
   float   scale;             /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
   const int64_t *ctx_off;    /* [B]   pool offset of each context */
@@ -138,7 +140,8 @@ ippd_status_t ippd_load_segments(const ippd_batch_t *batch, const void *k_raw,
 
 /*
  * Decode-step rotation and append (Sec. 4.1 virtual position of answer
- * tokens; Sec. 4.2 "appended with the correct virtual position").
+ * tokens; Sec. 4.2: each generated token re-enters the prompt at its virtual
+ * position for the next step).
  * For every active question i of prompt b, with s = seg_len[i] and
  * pos = ctx_len[b] + s:
  *   q_rot[i][h] = R(pos) q_new[i][h]        for all Hq heads,
@@ -152,9 +155,17 @@ ippd_status_t ippd_append_kv(const ippd_batch_t *batch, const void *q_new,
                              const void *k_new, const void *v_new, void *q_rot,
                              const ippd_kv_cache_t *kv, hipStream_t stream);
 
-/* Workspace bytes needed by ippd_decode_attention / standard_decode_attention
- * for this batch (depends only on host-side fields).  Returns 0 for an
- * invalid batch. */
+/*
+ * Workspace of the decode calls: device scratch holding arrival counters and
+ * the partial softmax states of the context chunks and segments.
+ * ippd_decode_workspace_bytes serves ippd_decode_attention and
+ * ippd_decode_step, standard_decode_workspace_bytes the two standard_* calls
+ * (sizes depend only on host-side fields; 0 means an invalid batch).
+ * A workspace must be 256-byte aligned and ZERO-FILLED before its first use;
+ * every call leaves its counters at zero again, so it can be reused by later
+ * calls on the same stream without clearing.  Calls that run concurrently
+ * need separate workspaces.
+ */
 size_t ippd_decode_workspace_bytes(const ippd_batch_t *batch);
 size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
 
@@ -170,8 +181,9 @@ size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
  * exactly.  lse[i][h] = natural-log sum of exp over the same logits
  * (optional, may be NULL).  out [Nt][Hq][D] and lse [Nt][Hq] are float32;
  * rows of inactive questions are not written.
- * workspace: device scratch of >= ippd_decode_workspace_bytes(batch) bytes,
- * 256-byte aligned, exclusive to this call until it completes.
+ * workspace: >= ippd_decode_workspace_bytes(batch) bytes (see above).
+ * One kernel launch: chunk partials are merged in-kernel by whichever work
+ * unit of a question group finishes last.
  */
 ippd_status_t ippd_decode_attention(const ippd_batch_t *batch, const void *q_rot,
                                     const ippd_kv_cache_t *kv, float *out, float *lse,
@@ -190,6 +202,30 @@ ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q
                                         const ippd_kv_cache_t *kv, float *out, float *lse,
                                         void *workspace, size_t workspace_bytes,
                                         hipStream_t stream);
+
+/*
+ * Fused decode step: ippd_append_kv followed by ippd_decode_attention, in
+ * ONE kernel launch.  q_new [Nt][Hq][D], k_new/v_new [Nt][Hkv][D] are the
+ * raw (pre-rotation) projections of the token each active question feeds
+ * this step.  The launch rotates them at virtual position
+ * ctx_len[b] + seg_len[i], appends the key/value to the segment, attends
+ * (context + segment including the new token) and advances seg_len[i].
+ * q_rot [Nt][Hq][D] receives the rotated queries, or may be NULL.  An active
+ * question whose segment is full (seg_len[i] == seg_capacity) sets
+ * IPPD_FLAG_SEGMENT_FULL and gets no output row.  workspace as for
+ * ippd_decode_attention.
+ */
+ippd_status_t ippd_decode_step(const ippd_batch_t *batch, const void *q_new, const void *k_new,
+                               const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,
+                               float *out, float *lse, void *workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* The standard baseline as one fused launch (append + per-question attention);
+ * workspace >= standard_decode_workspace_bytes(batch). */
+ippd_status_t standard_decode_step(const ippd_batch_t *batch, const void *q_new, const void *k_new,
+                                   const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,
+                                   float *out, float *lse, void *workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
 
 /* Static description of a status code. */
 const char *ippd_status_string(ippd_status_t status);

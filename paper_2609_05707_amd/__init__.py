@@ -18,4 +18,6 @@ from ._lib import (  # noqa: F401
     standard_decode_workspace_bytes,
     ippd_decode_attention,
     standard_decode_attention,
+    ippd_decode_step,
+    standard_decode_step,
 )

@@ -31,6 +31,7 @@ EXPORTED = [
     "ippd_load_context", "ippd_load_segments", "ippd_append_kv",
     "ippd_decode_workspace_bytes", "standard_decode_workspace_bytes",
     "ippd_decode_attention", "standard_decode_attention",
+    "ippd_decode_step", "standard_decode_step",
     "ippd_status_string", "ippd_last_hip_error", "ippd_version",
 ]
 
@@ -49,6 +50,7 @@ class IppdBatch(ctypes.Structure):
         ("max_ctx_len", c_int32),
         ("max_questions", c_int32),
         ("chunk_tokens", c_int32),
+        ("tile_rows", c_int32),
         ("rope_base", c_double),
         ("scale", c_float),
         ("ctx_off", c_void_p),
@@ -96,6 +98,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("ippd_decode_attention", "standard_decode_attention"):
         getattr(lib, name).argtypes = [P(IppdBatch), c_void_p, P(IppdKvCache), c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]
+        getattr(lib, name).restype = st
+    for name in ("ippd_decode_step", "standard_decode_step"):
+        getattr(lib, name).argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache),
+                                       c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
         getattr(lib, name).restype = st
     lib.ippd_status_string.argtypes = [c_int]
     lib.ippd_status_string.restype = ctypes.c_char_p
@@ -149,6 +155,21 @@ def standard_decode_attention(batch, q_rot, kv, out, lse, workspace, workspace_b
     _check("standard_decode_attention",
            load_library().standard_decode_attention(ctypes.byref(batch), q_rot, ctypes.byref(kv), out, lse,
                                                     workspace, workspace_bytes, stream))
+
+
+def ippd_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, workspace, workspace_bytes,
+                     stream) -> None:
+    _check("ippd_decode_step",
+           load_library().ippd_decode_step(ctypes.byref(batch), q_new, k_new, v_new, q_rot, ctypes.byref(kv),
+                                           out, lse, workspace, workspace_bytes, stream))
+
+
+def standard_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, workspace, workspace_bytes,
+                         stream) -> None:
+    _check("standard_decode_step",
+           load_library().standard_decode_step(ctypes.byref(batch), q_new, k_new, v_new, q_rot,
+                                               ctypes.byref(kv), out, lse, workspace, workspace_bytes,
+                                               stream))
 
 
 def raw_status(fn: str, *args) -> int:

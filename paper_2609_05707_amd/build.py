@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libippd.so")
 
-SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_attention.hip"]
+SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

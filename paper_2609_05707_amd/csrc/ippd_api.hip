@@ -13,7 +13,7 @@ thread_local int g_last_hip_error = 0;
 
 constexpr int kTargetUnits = 1024;   // context units aimed for per launch (4 per CU)
 constexpr int kMinChunk = 128;
-constexpr int kMaxChunk = 16384;
+constexpr int kMaxChunk = 4096;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -24,13 +24,16 @@ ippd_status_t check_batch(const ippd_batch_t* bt) {
   if (bt->num_prompts < 1 || bt->num_questions < 0 || bt->num_q_heads < 1 || bt->num_kv_heads < 1)
     return IPPD_ERR_SHAPE;
   if (bt->num_q_heads % bt->num_kv_heads != 0) return IPPD_ERR_SHAPE;
-  if (bt->num_q_heads / bt->num_kv_heads > 64) return IPPD_ERR_SHAPE;
+  if (bt->num_q_heads / bt->num_kv_heads > ippd::kMaxGroup) return IPPD_ERR_SHAPE;
   if (bt->head_dim != 64 && bt->head_dim != 128) return IPPD_ERR_SHAPE;
   if (bt->ctx_pool_tokens < 0 || (bt->ctx_pool_tokens & 7)) return IPPD_ERR_SHAPE;
   if (bt->seg_capacity < 8 || (bt->seg_capacity & 7)) return IPPD_ERR_SHAPE;
   if (bt->max_ctx_len < 0 || bt->max_ctx_len > bt->ctx_pool_tokens) return IPPD_ERR_SHAPE;
   if (bt->max_questions < 1 || bt->max_questions > ippd::kMaxQuestionsPerPrompt) return IPPD_ERR_SHAPE;
   if (bt->chunk_tokens < 0 || (bt->chunk_tokens & 31)) return IPPD_ERR_SHAPE;
+  if (bt->tile_rows != 0 && bt->tile_rows != 16 && bt->tile_rows != 32 && bt->tile_rows != 64 &&
+      bt->tile_rows != 128)
+    return IPPD_ERR_SHAPE;
   if (!(bt->rope_base > 0.0) || !isfinite(bt->rope_base)) return IPPD_ERR_SHAPE;
   if (!isfinite(bt->scale)) return IPPD_ERR_SHAPE;
   if (!bt->ctx_off || !bt->ctx_len || !bt->q_start || !bt->seg_len || !bt->active || !bt->err_flag)
@@ -44,42 +47,63 @@ float softmax_scale(const ippd_batch_t* bt) {
 
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-// Launch plan of a decode-attention call.  Depends only on host fields, so the
+// theta_j = base^(-2j/D) in fp64, the rotation frequencies of pair j.
+void fill_inv_freq(const ippd_batch_t* bt, double* out) {
+  const int half = bt->head_dim / 2;
+  for (int j = 0; j < ippd::kMaxHalfDim; ++j)
+    out[j] = j < half ? pow(bt->rope_base, -2.0 * j / bt->head_dim) : 0.0;
+}
+
+// Launch plan of a decode call.  Depends only on host fields, so the
 // workspace query and the launch agree.
-bool plan_attention(const ippd_batch_t* bt, bool shared, ippd::AttnPlan* pl) {
+bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   if (check_batch(bt) != IPPD_OK) return false;
   const int G = bt->num_q_heads / bt->num_kv_heads;
   const int64_t max_rows = shared ? static_cast<int64_t>(bt->max_questions) * G : G;
-  const int rb = max_rows <= 16 ? 1 : (max_rows <= 32 ? 2 : 4);
-  const int rw = 16 * rb;
+  // rows per context unit: 16 -> four waves split the tokens of one 16-row
+  // block; 32/64/128 -> 2/4/8 waves each own a 16-row block of a shared tile
+  int rw = bt->tile_rows;
+  if (rw == 0) rw = max_rows <= 16 ? 16 : (max_rows <= 32 ? 32 : (max_rows <= 64 ? 64 : 128));
+  if (!shared) rw = 16;
+  const bool row_split = rw > 16;
+  const int waves = row_split ? rw / 16 : 4;
   const int nrg = shared ? static_cast<int>((max_rows + rw - 1) / rw) : 1;
+  const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
+                                  : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   int chunk = bt->chunk_tokens;
   if (chunk == 0) {
-    const int64_t streams = shared ? static_cast<int64_t>(bt->num_prompts) * nrg : bt->num_questions;
-    const int64_t work = streams * bt->max_ctx_len * bt->num_kv_heads;
+    const int64_t work = n_groups * nrg * bt->max_ctx_len;
     int64_t ch = (work + kTargetUnits - 1) / kTargetUnits;
     ch = (ch + 31) / 32 * 32;
     ch = ch < kMinChunk ? kMinChunk : (ch > kMaxChunk ? kMaxChunk : ch);
     chunk = static_cast<int>(ch);
   }
   const int max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
-  const int64_t ctx_per_g = shared ? static_cast<int64_t>(bt->num_prompts) * max_chunks * nrg
-                                   : static_cast<int64_t>(bt->num_questions) * max_chunks;
-  const int64_t units_per_g = ctx_per_g + bt->num_questions;
-  const int64_t n_units = units_per_g * bt->num_kv_heads;
-  if (n_units > (1ll << 30)) return false;
+  const int64_t ctx_upg = static_cast<int64_t>(max_chunks) * nrg;
+  const int64_t seg_upg = shared ? (bt->max_questions + waves - 1) / waves : 1;
+  const int64_t upg = ctx_upg + seg_upg;
+  const int64_t gps = (n_groups + 7) / 8;
+  const int64_t per_slice = gps * upg;
+  if (per_slice * 8 > (1ll << 30) || n_groups == 0) return false;
   pl->shared = shared ? 1 : 0;
-  pl->rb = rb;
+  pl->waves = waves;
+  pl->row_split = row_split ? 1 : 0;
+  pl->rw = rw;
   pl->nrg = nrg;
   pl->chunk = chunk;
   pl->max_chunks = max_chunks;
-  pl->ctx_per_g = static_cast<int>(ctx_per_g);
-  pl->units_per_g = static_cast<int>(units_per_g);
-  pl->n_units = static_cast<int>(n_units);
-  pl->grid = static_cast<int>((n_units + 7) / 8 * 8);
+  pl->ctx_units_per_group = static_cast<int>(ctx_upg);
+  pl->seg_units_per_group = static_cast<int>(seg_upg);
+  pl->units_per_group = static_cast<int>(upg);
+  pl->n_groups = static_cast<int>(n_groups);
+  pl->groups_per_slice = static_cast<int>(gps);
+  pl->per_slice = static_cast<int>(per_slice);
+  pl->grid = static_cast<int>(per_slice * 8);
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
-  pl->workspace_bytes = round256(pl->part_slots * bt->head_dim * sizeof(float)) +
-                        round256(pl->part_slots * 2 * sizeof(float));
+  pl->counters = static_cast<size_t>(n_groups) * seg_upg + bt->num_questions;
+  pl->off_acc = round256(pl->counters * sizeof(uint32_t));
+  pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
+  pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
   return true;
 }
 
@@ -89,40 +113,54 @@ ippd_status_t hip_status(hipError_t e) {
   return IPPD_ERR_HIP;
 }
 
-ippd_status_t decode_attention(const ippd_batch_t* bt, bool shared, const void* q_rot,
-                               const ippd_kv_cache_t* kv, float* out, float* lse,
-                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+// Shared body of the four decode entry points.  fused: q_new/k_new/v_new are
+// raw token inputs that this launch rotates and appends (q_rot optional
+// output); otherwise q_rot holds rotated queries and the segment already
+// contains the step's token.
+ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void* q_new,
+                     const void* k_new, const void* v_new, const void* q_rot_in, void* q_rot_out,
+                     const ippd_kv_cache_t* kv, float* out, float* lse, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream) {
   ippd_status_t st = check_batch(bt);
   if (st != IPPD_OK) return st;
-  if (!kv || !q_rot || !out || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt)
-    return IPPD_ERR_NULL;
-  if (!aligned16(q_rot) || !aligned16(out) || !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) ||
-      !aligned16(kv->seg_k) || !aligned16(kv->seg_vt) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3)))
+  if (!kv || !out || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt) return IPPD_ERR_NULL;
+  if (fused ? (!q_new || !k_new || !v_new) : !q_rot_in) return IPPD_ERR_NULL;
+  if (!aligned16(out) || !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) ||
+      !aligned16(kv->seg_vt) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3)))
     return IPPD_ERR_ALIGN;
-  ippd::AttnPlan pl;
-  if (!plan_attention(bt, shared, &pl)) return IPPD_ERR_SHAPE;
+  if (fused ? (!aligned16(q_new) || !aligned16(k_new) || !aligned16(v_new) || (q_rot_out && !aligned16(q_rot_out)))
+            : !aligned16(q_rot_in))
+    return IPPD_ERR_ALIGN;
+  ippd::StepPlan pl;
+  if (!plan_step(bt, shared, &pl)) return IPPD_ERR_SHAPE;
   if (bt->num_questions == 0) return IPPD_OK;
   if (!workspace || workspace_bytes < pl.workspace_bytes) return IPPD_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) & 255u) return IPPD_ERR_ALIGN;
 
-  ippd::AttnParams p;
+  ippd::StepParams p;
+  p.q_new = q_new; p.k_new = k_new; p.v_new = v_new;
+  p.q_rot_in = q_rot_in; p.q_rot_out = q_rot_out;
   p.ctx_k = kv->ctx_k; p.ctx_vt = kv->ctx_vt; p.seg_k = kv->seg_k; p.seg_vt = kv->seg_vt;
-  p.q = q_rot;
   p.ctx_off = bt->ctx_off; p.ctx_len = bt->ctx_len; p.q_start = bt->q_start;
   p.seg_len = bt->seg_len; p.active = bt->active; p.err_flag = bt->err_flag;
-  p.part_acc = static_cast<float*>(workspace);
-  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                       round256(pl.part_slots * bt->head_dim * sizeof(float)));
   p.out = out; p.lse = lse;
+  char* ws = static_cast<char*>(workspace);
+  p.counters = reinterpret_cast<uint32_t*>(ws);
+  p.part_acc = reinterpret_cast<float*>(ws + pl.off_acc);
+  p.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   p.pool = bt->ctx_pool_tokens;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hq = bt->num_q_heads; p.Hkv = bt->num_kv_heads;
   p.G = bt->num_q_heads / bt->num_kv_heads; p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
-  p.shared = pl.shared; p.nrg = pl.nrg; p.chunk = pl.chunk; p.max_chunks = pl.max_chunks;
-  p.ctx_per_g = pl.ctx_per_g; p.units_per_g = pl.units_per_g; p.n_units = pl.n_units; p.grid = pl.grid;
+  p.shared = pl.shared; p.fused = fused ? 1 : 0; p.rw = pl.rw; p.nrg = pl.nrg; p.chunk = pl.chunk;
+  p.max_chunks = pl.max_chunks;
+  p.ctx_units_per_group = pl.ctx_units_per_group; p.seg_units_per_group = pl.seg_units_per_group;
+  p.units_per_group = pl.units_per_group; p.n_groups = pl.n_groups;
+  p.groups_per_slice = pl.groups_per_slice; p.per_slice = pl.per_slice;
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
-  return hip_status(ippd::launch_attention(bt->dtype, pl.rb, p, stream));
+  fill_inv_freq(bt, p.inv_freq);
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.row_split != 0, pl.grid, p, stream));
 }
 
 }  // namespace
@@ -140,7 +178,8 @@ ippd_status_t ippd_load_context(const ippd_batch_t* bt, const void* k_raw, const
   p.k_raw = k_raw; p.v_raw = v_raw; p.ctx_k = kv->ctx_k; p.ctx_vt = kv->ctx_vt;
   p.ctx_off = bt->ctx_off; p.ctx_len = bt->ctx_len; p.err_flag = bt->err_flag;
   p.pool = bt->ctx_pool_tokens; p.B = bt->num_prompts; p.Hkv = bt->num_kv_heads; p.D = bt->head_dim;
-  p.max_ctx_len = bt->max_ctx_len; p.base = bt->rope_base;
+  p.max_ctx_len = bt->max_ctx_len;
+  fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_load_context(bt->dtype, p, stream));
 }
 
@@ -156,7 +195,8 @@ ippd_status_t ippd_load_segments(const ippd_batch_t* bt, const void* k_raw, cons
   p.k_raw = k_raw; p.v_raw = v_raw; p.init_len = init_len; p.seg_k = kv->seg_k; p.seg_vt = kv->seg_vt;
   p.ctx_len = bt->ctx_len; p.q_start = bt->q_start; p.seg_len = bt->seg_len; p.err_flag = bt->err_flag;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hkv = bt->num_kv_heads; p.D = bt->head_dim;
-  p.seg_cap = bt->seg_capacity; p.base = bt->rope_base;
+  p.seg_cap = bt->seg_capacity;
+  fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_load_segments(bt->dtype, p, stream));
 }
 
@@ -175,31 +215,49 @@ ippd_status_t ippd_append_kv(const ippd_batch_t* bt, const void* q_new, const vo
   p.ctx_len = bt->ctx_len; p.q_start = bt->q_start; p.seg_len = bt->seg_len;
   p.active = bt->active; p.err_flag = bt->err_flag;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hq = bt->num_q_heads; p.Hkv = bt->num_kv_heads;
-  p.D = bt->head_dim; p.seg_cap = bt->seg_capacity; p.base = bt->rope_base;
+  p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
+  fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_append(bt->dtype, p, stream));
 }
 
 size_t ippd_decode_workspace_bytes(const ippd_batch_t* bt) {
-  ippd::AttnPlan pl;
-  return plan_attention(bt, true, &pl) ? pl.workspace_bytes : 0;
+  ippd::StepPlan pl;
+  return plan_step(bt, true, &pl) ? pl.workspace_bytes : 0;
 }
 
 size_t standard_decode_workspace_bytes(const ippd_batch_t* bt) {
-  ippd::AttnPlan pl;
-  return plan_attention(bt, false, &pl) ? pl.workspace_bytes : 0;
+  ippd::StepPlan pl;
+  return plan_step(bt, false, &pl) ? pl.workspace_bytes : 0;
 }
 
 ippd_status_t ippd_decode_attention(const ippd_batch_t* bt, const void* q_rot,
                                     const ippd_kv_cache_t* kv, float* out, float* lse,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return decode_attention(bt, true, q_rot, kv, out, lse, workspace, workspace_bytes, stream);
+  return decode(bt, true, false, nullptr, nullptr, nullptr, q_rot, nullptr, kv, out, lse, workspace,
+                workspace_bytes, stream);
 }
 
 ippd_status_t standard_decode_attention(const ippd_batch_t* bt, const void* q_rot,
                                         const ippd_kv_cache_t* kv, float* out, float* lse,
                                         void* workspace, size_t workspace_bytes,
                                         hipStream_t stream) {
-  return decode_attention(bt, false, q_rot, kv, out, lse, workspace, workspace_bytes, stream);
+  return decode(bt, false, false, nullptr, nullptr, nullptr, q_rot, nullptr, kv, out, lse, workspace,
+                workspace_bytes, stream);
+}
+
+ippd_status_t ippd_decode_step(const ippd_batch_t* bt, const void* q_new, const void* k_new,
+                               const void* v_new, void* q_rot, const ippd_kv_cache_t* kv, float* out,
+                               float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return decode(bt, true, true, q_new, k_new, v_new, nullptr, q_rot, kv, out, lse, workspace,
+                workspace_bytes, stream);
+}
+
+ippd_status_t standard_decode_step(const ippd_batch_t* bt, const void* q_new, const void* k_new,
+                                   const void* v_new, void* q_rot, const ippd_kv_cache_t* kv,
+                                   float* out, float* lse, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  return decode(bt, false, true, q_new, k_new, v_new, nullptr, q_rot, kv, out, lse, workspace,
+                workspace_bytes, stream);
 }
 
 const char* ippd_status_string(ippd_status_t s) {
@@ -217,6 +275,6 @@ const char* ippd_status_string(ippd_status_t s) {
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 100; }
+int ippd_version(void) { return 200; }
 
 }  // extern "C"

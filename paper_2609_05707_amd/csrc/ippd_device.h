@@ -11,7 +11,6 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef uint16_t u16x8_t __attribute__((ext_vector_type(8)));
 
-constexpr int kWave = 64;
 constexpr int kFlagSegmentFull = 1;
 constexpr int kFlagBadLayout = 2;
 
@@ -35,6 +34,24 @@ template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t x) { retu
 template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f32_to_bf16(x); }
+
+// cos/sin of pos * theta.  The angle is formed and reduced to [-pi, pi] in
+// fp64 (2*pi split hi + lo), then evaluated with fp32 sincos: the result is
+// accurate to a few 1e-7 for any position, where an fp32 angle would be off
+// by ~pos * 6e-8 rad.
+__device__ __forceinline__ void rope_cos_sin(int64_t pos, double theta, float& c, float& s) {
+  const double ang = static_cast<double>(pos) * theta;
+  const double k = rint(ang * 0.15915494309189535);
+  const double r = fma(-k, 6.283185307179586, ang) - k * 2.4492935982947064e-16;
+  sincosf(static_cast<float>(r), &s, &c);
+}
+
+// Rotate one pair (a, b) = (x_j, x_{j+D/2}) by (c, s) = (cos, sin); written with
+// explicit fmaf so every call site rounds identically.
+__device__ __forceinline__ void rope_rotate(float a, float b, float c, float s, float& x, float& y) {
+  x = fmaf(a, c, -(b * s));
+  y = fmaf(b, c, a * s);
+}
 
 // Butterfly partners across the four 16-lane rows of a wave64, via the gfx950
 // permlane swaps.  After swapping a value with itself, the two results hold

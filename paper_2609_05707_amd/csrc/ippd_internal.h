@@ -2,18 +2,21 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace ippd {
 
 constexpr int kMaxQuestionsPerPrompt = 1024;   // LDS list of a prompt's active questions
+constexpr int kMaxGroup = 16;                  // query heads per kv head (one MFMA row block)
+constexpr int kMaxHalfDim = 64;                // D/2 for D <= 128
 
 struct LoadContextParams {
   const void* k_raw; const void* v_raw;     // [pool][Hkv][D]
   void* ctx_k; void* ctx_vt;
   const int64_t* ctx_off; const int32_t* ctx_len; int32_t* err_flag;
   int64_t pool; int B, Hkv, D, max_ctx_len;
-  double base;
+  double inv_freq[kMaxHalfDim];
 };
 
 struct LoadSegmentsParams {
@@ -22,7 +25,7 @@ struct LoadSegmentsParams {
   void* seg_k; void* seg_vt;
   const int32_t* ctx_len; const int32_t* q_start; int32_t* seg_len; int32_t* err_flag;
   int B, Nt, Hkv, D, seg_cap;
-  double base;
+  double inv_freq[kMaxHalfDim];
 };
 
 struct AppendParams {
@@ -31,42 +34,57 @@ struct AppendParams {
   const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   int B, Nt, Hq, Hkv, D, seg_cap;
-  double base;
+  double inv_freq[kMaxHalfDim];
 };
 
-// One decode-attention launch plan (shared by IPPD and the standard baseline).
-struct AttnPlan {
-  int shared;        // 1: a context unit serves every active question of its prompt
-  int rb;            // 16-row MFMA row blocks per wave (1, 2 or 4)
-  int nrg;           // row groups of 16*rb rows per (prompt, kv head) in shared mode
-  int chunk;         // context tokens per unit (multiple of 32)
-  int max_chunks;    // ceil(max_ctx_len / chunk)
-  int ctx_per_g;     // context units per kv head
-  int units_per_g;   // context + segment units per kv head
-  int n_units;       // units_per_g * Hkv
-  int grid;          // n_units rounded up to a multiple of 8 (one slice per XCD)
-  size_t part_slots;       // (max_chunks + 1) * Nt * Hq
-  size_t workspace_bytes;  // part_slots * (D + 2) * 4, 256-byte rounded pieces
+// Launch plan of one decode-attention call.  Work is grouped per
+// (prompt, kv head) in IPPD mode and per (question, kv head) in the standard
+// baseline; a group owns its context units and its segment units, and the
+// groups are dealt in contiguous runs to the 8 workgroup slices (XCDs).
+struct StepPlan {
+  int shared;              // 1: IPPD, context units serve all active questions of a prompt
+  int waves;               // waves per workgroup (questions per segment unit in IPPD mode)
+  int row_split;           // 1: waves split a context unit's rows (16 each), 0: its tokens
+  int rw;                  // query rows per context unit
+  int nrg;                 // row groups per group
+  int chunk;               // context tokens per context unit (multiple of 32)
+  int max_chunks;          // ceil(max_ctx_len / chunk)
+  int ctx_units_per_group; // max_chunks * nrg
+  int seg_units_per_group; // segment units (one question per wave) per group
+  int units_per_group;
+  int n_groups;
+  int groups_per_slice;
+  int per_slice;
+  int grid;                // 8 * per_slice workgroups
+  size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states
+  size_t counters;         // n_groups * seg_units_per_group + Nt 32-bit counters
+  size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
+  size_t workspace_bytes;
 };
 
-struct AttnParams {
-  const void* ctx_k; const void* ctx_vt; const void* seg_k; const void* seg_vt;
-  const void* q;     // q_rot [Nt][Hq][D]
+struct StepParams {
+  const void* q_new; const void* k_new; const void* v_new;   // fused step: raw token inputs
+  const void* q_rot_in;                                        // attention only: rotated queries
+  void* q_rot_out;                                             // fused step: rotated queries (or null)
+  void* ctx_k; void* ctx_vt; void* seg_k; void* seg_vt;
   const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start;
-  const int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
-  float* part_acc;   // [part_slots][D]
-  float* part_ml;    // [part_slots][2]  (running max in raw logit units, sum)
+  int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   float* out; float* lse;
+  uint32_t* counters;      // [n_groups * seg_units_per_group] arrivals, then [Nt] per-question
+  float* part_acc;         // [part_slots][D]
+  float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
-  int shared, nrg, chunk, max_chunks, ctx_per_g, units_per_g, n_units, grid;
-  float c;           // scale * log2(e)
+  int shared, fused, rw, nrg, chunk, max_chunks;
+  int ctx_units_per_group, seg_units_per_group, units_per_group, n_groups, groups_per_slice, per_slice;
+  float c;                 // scale * log2(e)
   float scale;
+  double inv_freq[kMaxHalfDim];
 };
 
 hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s);
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
-hipError_t launch_attention(int dtype, int rb, const AttnParams& p, hipStream_t s);
+hipError_t launch_step(int dtype, int waves, bool row_split, int grid, const StepParams& p, hipStream_t s);
 
 }  // namespace ippd

@@ -1,36 +1,30 @@
-// Rotary embedding at virtual positions, KV append, and cache loaders.
+// Rotary embedding at virtual positions: decode-step append and cache loaders.
 //
 // Positions follow the virtual-position rule of Sec. 4.1: a context token t
 // sits at t (instruction folded into the context), segment slot t of a
 // question of prompt b at ctx_len[b] + t, and the token fed at a decode step
-// at ctx_len[b] + seg_len[i].  Angles pos * theta_j are formed in fp64 (a
-// fp32 product loses ~pos * 6e-8 rad), rotated values are rounded once to
-// the cache dtype.
+// at ctx_len[b] + seg_len[i].  theta_j = base^(-2j/D) comes from the host in
+// fp64; cos/sin use the fp64-reduced angle (rope_cos_sin).
 #include "ippd_device.h"
 #include "ippd_internal.h"
 
 namespace ippd {
 
-// cos/sin(pos * theta_j) for j < D/2 into LDS, theta_j = base^(-2j/D).
-__device__ __forceinline__ void rope_table(double* s_cos, double* s_sin, int D, double base,
-                                           int64_t pos) {
-  for (int j = threadIdx.x; j < D / 2; j += blockDim.x) {
-    double theta = pow(base, -2.0 * j / D);
-    double ang = static_cast<double>(pos) * theta;
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    s_cos[j] = cs;
-    s_sin[j] = sn;
-  }
-}
-
+// Rotate 8 consecutive pairs (x[j], x[j + D/2]) for j = j0..j0+7.
 template <typename T>
-__device__ __forceinline__ void rotate_pair(const T* src, T* dst, int j, int half,
-                                            double cs, double sn) {
-  double x = to_f32<T>(src[j]);
-  double y = to_f32<T>(src[j + half]);
-  dst[j] = from_f32<T>(static_cast<float>(x * cs - y * sn));
-  dst[j + half] = from_f32<T>(static_cast<float>(y * cs + x * sn));
+__device__ __forceinline__ void rotate8(const T* __restrict__ src, T* __restrict__ dst, int j0, int half,
+                                        const float2* cs) {
+  float a[8], bb[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) { a[u] = to_f32<T>(src[j0 + u]); bb[u] = to_f32<T>(src[j0 + half + u]); }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float2 c = cs[j0 + u];
+    float x, y;
+    rope_rotate(a[u], bb[u], c.x, c.y, x, y);
+    dst[j0 + u] = from_f32<T>(x);
+    dst[j0 + half + u] = from_f32<T>(y);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -38,7 +32,7 @@ __device__ __forceinline__ void rotate_pair(const T* src, T* dst, int j, int hal
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
-  __shared__ double s_cos[64], s_sin[64];
+  __shared__ float2 s_cs[kMaxHalfDim];
   const int i = blockIdx.x;
   if (i >= p.Nt || !p.active[i]) return;
   const int b = prompt_of(p.q_start, p.B, i);
@@ -49,26 +43,31 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
   }
   const int D = p.D, half = D / 2;
   const int64_t pos = static_cast<int64_t>(p.ctx_len[b]) + s;
-  rope_table(s_cos, s_sin, D, p.base, pos);
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    float c, sn;
+    rope_cos_sin(pos, p.inv_freq[j], c, sn);
+    s_cs[j] = make_float2(c, sn);
+  }
   __syncthreads();
 
-  const T* qn = static_cast<const T*>(p.q_new);
-  const T* kn = static_cast<const T*>(p.k_new);
-  const T* vn = static_cast<const T*>(p.v_new);
-  T* qr = static_cast<T*>(p.q_rot);
-  T* sk = static_cast<T*>(p.seg_k);
-  T* svt = static_cast<T*>(p.seg_vt);
+  const T* __restrict__ qn = static_cast<const T*>(p.q_new);
+  const T* __restrict__ kn = static_cast<const T*>(p.k_new);
+  const T* __restrict__ vn = static_cast<const T*>(p.v_new);
+  T* __restrict__ qr = static_cast<T*>(p.q_rot);
+  T* __restrict__ sk = static_cast<T*>(p.seg_k);
+  T* __restrict__ svt = static_cast<T*>(p.seg_vt);
+  const int oct = half / 8;                    // groups of 8 pairs per head
   const int heads = p.Hq + p.Hkv;
-  for (int e = threadIdx.x; e < heads * half; e += blockDim.x) {
-    const int hh = e / half, j = e - hh * half;
+  for (int e = threadIdx.x; e < heads * oct; e += blockDim.x) {
+    const int hh = e / oct, j0 = (e - hh * oct) * 8;
     if (hh < p.Hq) {
       const int64_t off = (static_cast<int64_t>(i) * p.Hq + hh) * D;
-      rotate_pair<T>(qn + off, qr + off, j, half, s_cos[j], s_sin[j]);
+      rotate8<T>(qn + off, qr + off, j0, half, s_cs);
     } else {
       const int g = hh - p.Hq;
       const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D;
       const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * p.seg_cap + s) * D;
-      rotate_pair<T>(kn + src, sk + dst, j, half, s_cos[j], s_sin[j]);
+      rotate8<T>(kn + src, sk + dst, j0, half, s_cs);
     }
   }
   for (int e = threadIdx.x; e < p.Hkv * D; e += blockDim.x) {
@@ -102,20 +101,21 @@ __global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, 
   if (t0 >= len) return;
   const int nt = min(kLoadTile, len - t0);
   const int D = p.D, half = D / 2;
-  const T* kr = static_cast<const T*>(p.k_raw);
-  const T* vr = static_cast<const T*>(p.v_raw);
-  T* ck = static_cast<T*>(p.ctx_k);
-  T* cvt = static_cast<T*>(p.ctx_vt);
-  // keys: rotate at position t (pair per thread; fp64 angle per pair)
+  const T* __restrict__ kr = static_cast<const T*>(p.k_raw);
+  const T* __restrict__ vr = static_cast<const T*>(p.v_raw);
+  T* __restrict__ ck = static_cast<T*>(p.ctx_k);
+  T* __restrict__ cvt = static_cast<T*>(p.ctx_vt);
   for (int e = threadIdx.x; e < nt * half; e += blockDim.x) {
     const int tt = e / half, j = e - tt * half;
     const int t = t0 + tt;
-    const double theta = pow(p.base, -2.0 * j / D);
-    double sn, cs;
-    sincos(static_cast<double>(t) * theta, &sn, &cs);
+    float c, sn;
+    rope_cos_sin(t, p.inv_freq[j], c, sn);
     const int64_t src = ((off + t) * p.Hkv + g) * D;
     const int64_t dst = (static_cast<int64_t>(g) * p.pool + off + t) * D;
-    rotate_pair<T>(kr + src, ck + dst, j, half, cs, sn);
+    float x, y;
+    rope_rotate(to_f32<T>(kr[src + j]), to_f32<T>(kr[src + j + half]), c, sn, x, y);
+    ck[dst + j] = from_f32<T>(x);
+    ck[dst + j + half] = from_f32<T>(y);
   }
   // values: transpose a [tokens][D] tile into [D][tokens] through LDS
   for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
@@ -150,19 +150,21 @@ __global__ __launch_bounds__(256) void load_segments_kernel(LoadSegmentsParams p
   const int nt = min(kLoadTile, n - t0);
   const int D = p.D, half = D / 2;
   const int64_t base_pos = p.ctx_len[b];
-  const T* kr = static_cast<const T*>(p.k_raw);
-  const T* vr = static_cast<const T*>(p.v_raw);
-  T* sk = static_cast<T*>(p.seg_k);
-  T* svt = static_cast<T*>(p.seg_vt);
+  const T* __restrict__ kr = static_cast<const T*>(p.k_raw);
+  const T* __restrict__ vr = static_cast<const T*>(p.v_raw);
+  T* __restrict__ sk = static_cast<T*>(p.seg_k);
+  T* __restrict__ svt = static_cast<T*>(p.seg_vt);
   for (int e = threadIdx.x; e < nt * half; e += blockDim.x) {
     const int tt = e / half, j = e - tt * half;
     const int t = t0 + tt;
-    const double theta = pow(p.base, -2.0 * j / D);
-    double sn, cs;
-    sincos(static_cast<double>(base_pos + t) * theta, &sn, &cs);
+    float c, sn;
+    rope_cos_sin(base_pos + t, p.inv_freq[j], c, sn);
     const int64_t src = ((static_cast<int64_t>(i) * p.seg_cap + t) * p.Hkv + g) * D;
     const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * p.seg_cap + t) * D;
-    rotate_pair<T>(kr + src, sk + dst, j, half, cs, sn);
+    float x, y;
+    rope_rotate(to_f32<T>(kr[src + j]), to_f32<T>(kr[src + j + half]), c, sn, x, y);
+    sk[dst + j] = from_f32<T>(x);
+    sk[dst + j + half] = from_f32<T>(y);
   }
   for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
     const int tt = e / D, d = e - tt * D;

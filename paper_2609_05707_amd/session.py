@@ -34,7 +34,7 @@ class DecodeBatch:
     def __init__(self, ctx_len: Sequence[int], q_count: Sequence[int], hq: int, hkv: int,
                  head_dim: int, dtype: str, seg_capacity: int, rope_base: float = 10000.0,
                  scale: float = 0.0, chunk_tokens: int = 0, max_questions: Optional[int] = None,
-                 layers: int = 1, device: str = "cuda"):
+                 layers: int = 1, tile_rows: int = 0, device: str = "cuda"):
         self.device = torch.device(device)
         self.dtype = dtype
         self.tdtype = torch_dtype(dtype)
@@ -80,6 +80,7 @@ class DecodeBatch:
             bt.max_ctx_len = self.max_ctx_len
             bt.max_questions = self.max_questions
             bt.chunk_tokens = chunk_tokens
+            bt.tile_rows = tile_rows
             bt.rope_base = rope_base
             bt.scale = scale
             bt.ctx_off = self.d_ctx_off.data_ptr()
@@ -97,8 +98,9 @@ class DecodeBatch:
             self.caches.append(kv)
         self.ws_ippd_bytes = L.ippd_decode_workspace_bytes(self.batches[0])
         self.ws_std_bytes = L.standard_decode_workspace_bytes(self.batches[0])
-        self.ws_ippd = torch.empty(max(self.ws_ippd_bytes, 256), dtype=torch.uint8, device=dev)
-        self.ws_std = torch.empty(max(self.ws_std_bytes, 256), dtype=torch.uint8, device=dev)
+        # zero-filled once: the library keeps its arrival counters at zero between calls
+        self.ws_ippd = torch.zeros(max(self.ws_ippd_bytes, 256), dtype=torch.uint8, device=dev)
+        self.ws_std = torch.zeros(max(self.ws_std_bytes, 256), dtype=torch.uint8, device=dev)
         self.q_rot = torch.empty(nt, hq, head_dim, dtype=td, device=dev)
         self.out = torch.empty(nt, hq, head_dim, dtype=torch.float32, device=dev)
         self.lse = torch.empty(nt, hq, dtype=torch.float32, device=dev)
@@ -177,3 +179,18 @@ class DecodeBatch:
             L.ippd_decode_attention(self.batches[layer], q_rot.data_ptr(), self.caches[layer],
                                     out.data_ptr(), lse_ptr, self.ws_ippd.data_ptr(),
                                     self.ws_ippd_bytes, self.stream())
+
+    def decode_step(self, layer: int, q_new: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                    standard: bool = False, q_rot: Optional[torch.Tensor] = None,
+                    out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                    write_q_rot: bool = True, with_lse: bool = True) -> None:
+        """Fused step: rotate + append + attention in one launch."""
+        q_rot = self.q_rot if q_rot is None else q_rot
+        out = self.out if out is None else out
+        lse = self.lse if lse is None else lse
+        qr = q_rot.data_ptr() if write_q_rot else None
+        lse_ptr = lse.data_ptr() if with_lse else None
+        fn = L.standard_decode_step if standard else L.ippd_decode_step
+        ws, wsb = (self.ws_std, self.ws_std_bytes) if standard else (self.ws_ippd, self.ws_ippd_bytes)
+        fn(self.batches[layer], q_new.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), qr, self.caches[layer],
+           out.data_ptr(), lse_ptr, ws.data_ptr(), wsb, self.stream())

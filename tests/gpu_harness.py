@@ -32,12 +32,12 @@ class GpuRun:
 
 
 def make_batch(st: W.Structure, layers: int = 1, chunk_tokens: int = 0, extra_cap: int = 0,
-               max_questions: Optional[int] = None) -> DecodeBatch:
+               max_questions: Optional[int] = None, tile_rows: int = 0) -> DecodeBatch:
     wl = st.wl
     cap = int(st.seg_len0.max() if st.num_questions else 1) + wl.steps + extra_cap
     return DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim,
                        wl.dtype, cap, rope_base=wl.rope_base, chunk_tokens=chunk_tokens,
-                       max_questions=max_questions, layers=layers)
+                       max_questions=max_questions, layers=layers, tile_rows=tile_rows)
 
 
 def load_layer(db: DecodeBatch, st: W.Structure, layer_slot: int, kv: W.LayerKV) -> None:
@@ -47,21 +47,26 @@ def load_layer(db: DecodeBatch, st: W.Structure, layer_slot: int, kv: W.LayerKV)
 
 def run_gpu(st: W.Structure, steps: Iterable[int], record: Sequence[int], layer: int = 0,
             chunk_tokens: int = 0, standard: bool = False, sentinel: Optional[float] = None,
-            db: Optional[DecodeBatch] = None, kv: Optional[W.LayerKV] = None) -> GpuRun:
-    """Run the given steps (append + decode each) on one layer; copy out recorded steps."""
+            db: Optional[DecodeBatch] = None, kv: Optional[W.LayerKV] = None, fused: bool = False,
+            tile_rows: int = 0) -> GpuRun:
+    """Run the given steps on one layer, either as ippd_append_kv + decode attention or as
+    the fused single-launch step; copy out recorded steps."""
     if db is None:
-        db = make_batch(st, chunk_tokens=chunk_tokens)
+        db = make_batch(st, chunk_tokens=chunk_tokens, tile_rows=tile_rows)
         load_layer(db, st, 0, kv if kv is not None else W.layer_kv(st, layer))
     outs, lses, qrs = {}, {}, {}
     for t in steps:
         si = W.step_inputs(st, t, layer)
         db.set_active(si.active)
         q, k, v = db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new)
-        db.append(0, q, k, v)
         if sentinel is not None:
             db.out.fill_(sentinel)
             db.lse.fill_(sentinel)
-        db.decode(0, standard=standard)
+        if fused:
+            db.decode_step(0, q, k, v, standard=standard)
+        else:
+            db.append(0, q, k, v)
+            db.decode(0, standard=standard)
         if t in record:
             torch.cuda.synchronize()
             outs[t] = db.out[: st.num_questions].float().cpu().numpy().copy()
@@ -85,6 +90,22 @@ def oracle_steps(st: W.Structure, kv: W.LayerKV, steps: Iterable[int], record: S
                                             st.wl.rope_base, questions=qs)
         state.append(si.k_new, si.v_new, si.active)
     return res
+
+
+def counters_zero(db: DecodeBatch) -> bool:
+    """The arrival counters at the head of both workspaces are back at zero
+    (IPPD: B * Hkv * ceil(max_questions / 4) + Nt of them; baseline: Nt * Hkv + Nt)."""
+    torch.cuda.synchronize()
+    G = db.hq // db.hkv
+    rows = db.max_questions * G
+    tr = db.batches[0].tile_rows or (16 if rows <= 16 else 32 if rows <= 32 else 64 if rows <= 64 else 128)
+    waves = 4 if tr == 16 else tr // 16
+    n_ippd = db.B * db.hkv * ((db.max_questions + waves - 1) // waves) + db.Nt
+    n_std = db.Nt * db.hkv + db.Nt
+    ok = True
+    for ws, n in ((db.ws_ippd, n_ippd), (db.ws_std, n_std)):
+        ok &= bool(torch.all(ws[: 4 * n] == 0))
+    return ok
 
 
 def max_err(gpu: np.ndarray, ref: np.ndarray) -> float:

@@ -43,7 +43,7 @@ def valid_batch(**kw):
     bt.num_prompts, bt.num_questions, bt.num_q_heads, bt.num_kv_heads = 1, 4, 4, 2
     bt.head_dim, bt.dtype = 64, L.IPPD_DTYPE_F32
     bt.ctx_pool_tokens, bt.seg_capacity, bt.max_ctx_len, bt.max_questions = 256, 32, 256, 4
-    bt.chunk_tokens, bt.rope_base, bt.scale = 0, 10000.0, 0.0
+    bt.chunk_tokens, bt.tile_rows, bt.rope_base, bt.scale = 0, 0, 10000.0, 0.0
     for f in ("ctx_off", "ctx_len", "q_start", "seg_len", "active", "err_flag"):
         setattr(bt, f, FAKE)
     for k, v in kw.items():
@@ -81,6 +81,9 @@ def test_version_and_strings(lib):
     ("max_questions", 0, L.IPPD_ERR_SHAPE),
     ("max_questions", 2000, L.IPPD_ERR_SHAPE),
     ("chunk_tokens", 48, L.IPPD_ERR_SHAPE),         # not a multiple of 32
+    ("tile_rows", 24, L.IPPD_ERR_SHAPE),
+    ("tile_rows", 256, L.IPPD_ERR_SHAPE),
+    ("num_q_heads", 68, L.IPPD_ERR_SHAPE),          # 34 query heads per kv head
     ("rope_base", -1.0, L.IPPD_ERR_SHAPE),
     ("num_prompts", 0, L.IPPD_ERR_SHAPE),
     ("seg_len", None, L.IPPD_ERR_NULL),
@@ -122,11 +125,26 @@ def test_workspace_validation(lib):
 
 
 def test_workspace_formula(lib):
-    # (max_chunks + 1) * Nt * Hq slots of (D + 2) floats, each array 256-byte rounded.
+    # counters (one per segment group of 4 questions per group, one per question), then
+    # (max_chunks + 1) * Nt * Hq partial states of D + 2 floats; each piece 256-byte rounded.
     bt = valid_batch(chunk_tokens=64)
     slots = (256 // 64 + 1) * 4 * 4
     r = lambda x: (x + 255) // 256 * 256
-    assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == r(slots * 64 * 4) + r(slots * 2 * 4)
+    counters = 2 * 1 + 4            # B * Hkv groups x ceil(4 / 4) segment groups, + Nt
+    assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == \
+        r(counters * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
+    counters_std = 4 * 2 * 1 + 4    # Nt * Hkv groups x 1, + Nt
+    assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == \
+        r(counters_std * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
+
+
+def test_step_pointer_validation(lib):
+    bt = valid_batch()
+    kv = kv_cache()
+    args = lambda q, k, v: (ctypes.byref(bt), q, k, v, None, ctypes.byref(kv), FAKE, None, FAKE, 1 << 30, None)
+    assert lib.ippd_decode_step(*args(None, FAKE, FAKE)) == L.IPPD_ERR_NULL
+    assert lib.standard_decode_step(*args(FAKE, None, FAKE)) == L.IPPD_ERR_NULL
+    assert lib.ippd_decode_step(*args(FAKE, FAKE, MISALIGNED)) == L.IPPD_ERR_ALIGN
 
 
 def test_no_questions_is_a_noop(lib):

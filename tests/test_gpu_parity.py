@@ -9,7 +9,8 @@ import torch
 
 import workload as W
 from oracle import ippd as O
-from tests.gpu_harness import (load_layer, log, make_batch, max_err, oracle_steps, run_gpu)
+from tests.gpu_harness import (counters_zero, load_layer, log, make_batch, max_err, oracle_steps,
+                               run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -72,28 +73,57 @@ def ragged_workload(dtype, d=64, hq=8, hkv=2, steps=3, seed_id=200):
                              value_std=1.0 if dtype == "f32" else 0.5)
 
 
-@pytest.mark.parametrize("dtype,d,chunk", [("f32", 64, 0), ("f32", 128, 32), ("bf16", 128, 0),
-                                           ("bf16", 128, 64), ("bf16", 64, 32)])
-def test_small_ragged(dtype, d, chunk):
-    log(f"case: small ragged dtype={dtype} D={d} chunk={chunk}")
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("dtype,d,chunk,rows", [("f32", 64, 0, 0), ("f32", 128, 32, 16), ("bf16", 128, 0, 0),
+                                                ("bf16", 128, 64, 32), ("bf16", 64, 32, 64),
+                                                ("bf16", 128, 96, 16), ("bf16", 128, 160, 128),
+                                                ("f32", 64, 64, 128)])
+def test_small_ragged(dtype, d, chunk, rows, fused):
+    log(f"case: small ragged dtype={dtype} D={d} chunk={chunk} tile_rows={rows} fused={fused}")
     st = W.make_structure(ragged_workload(dtype, d))
     kv = W.layer_kv(st)
     steps = list(range(st.wl.steps))
-    gpu = run_gpu(st, steps, steps, chunk_tokens=chunk, kv=kv)
+    gpu = run_gpu(st, steps, steps, chunk_tokens=chunk, kv=kv, fused=fused, tile_rows=rows)
     ref = oracle_steps(st, kv, steps, steps)
     assert gpu.err == 0
-    check(st, gpu, ref, steps, f"ragged-{dtype}-{d}-{chunk}")
+    check(st, gpu, ref, steps, f"ragged-{dtype}-{d}-{chunk}-{rows}-{'fused' if fused else 'sep'}")
+    assert counters_zero(gpu.batch)
+    np.testing.assert_array_equal(gpu.batch.seg_len[0][: st.num_questions].cpu().numpy(),
+                                  st.seg_len_at(st.wl.steps))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_standard_baseline_matches_oracle(dtype):
-    log(f"case: standard baseline dtype={dtype}")
+def test_fused_step_equals_separate_calls(dtype):
+    """ippd_decode_step == ippd_append_kv + ippd_decode_attention (same rotation, same
+    partial regrouping), and its q_rot output equals the append's."""
+    log(f"case: fused vs separate dtype={dtype}")
+    st = W.make_structure(ragged_workload(dtype, 128, steps=3))
+    kv = W.layer_kv(st)
+    steps = list(range(3))
+    a = run_gpu(st, steps, steps, kv=kv, fused=False)
+    b = run_gpu(st, steps, steps, kv=kv, fused=True)
+    for t in steps:
+        act = st.active(t)
+        np.testing.assert_array_equal(a.out[t][act], b.out[t][act])
+        np.testing.assert_array_equal(a.q_rot[t][act], b.q_rot[t][act])
+    ka, kb = a.batch.seg_k[0].float().cpu().numpy(), b.batch.seg_k[0].float().cpu().numpy()
+    va, vb = a.batch.seg_vt[0].float().cpu().numpy(), b.batch.seg_vt[0].float().cpu().numpy()
+    for i, n in enumerate(st.seg_len_at(3)):           # filled slots only
+        np.testing.assert_array_equal(ka[i, :, :n], kb[i, :, :n])
+        np.testing.assert_array_equal(va[i, :, :, :n], vb[i, :, :, :n])
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_standard_baseline_matches_oracle(dtype, fused):
+    log(f"case: standard baseline dtype={dtype} fused={fused}")
     st = W.make_structure(ragged_workload(dtype, 128))
     kv = W.layer_kv(st)
     steps = list(range(st.wl.steps))
-    gpu = run_gpu(st, steps, steps, standard=True, kv=kv)
+    gpu = run_gpu(st, steps, steps, standard=True, kv=kv, fused=fused)
     ref = oracle_steps(st, kv, steps, steps)
-    check(st, gpu, ref, steps, f"standard-{dtype}")
+    check(st, gpu, ref, steps, f"standard-{dtype}-{'fused' if fused else 'sep'}")
+    assert counters_zero(gpu.batch)
 
 
 def test_inactive_rows_untouched_and_not_appended():
@@ -101,7 +131,7 @@ def test_inactive_rows_untouched_and_not_appended():
     st = W.make_structure(ragged_workload("bf16", 128, steps=4))
     kv = W.layer_kv(st)
     steps = list(range(4))
-    gpu = run_gpu(st, steps, steps, sentinel=-777.0, kv=kv)
+    gpu = run_gpu(st, steps, steps, sentinel=-777.0, kv=kv, fused=True)
     for t in steps:
         dead = ~st.active(t)
         assert np.all(gpu.out[t][dead] == -777.0) and np.all(gpu.lse[t][dead] == -777.0)
@@ -159,6 +189,22 @@ def test_empty_context_and_many_questions():
     sel = {0: list(range(0, 303, 7)) + [0, 1, 2]}
     ref = oracle_steps(st, kv, [0], [0], questions=sel)
     check(st, gpu, ref, [0], "empty-ctx/300q", qsel=sel)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_group_of_three_heads(fused):
+    """G = 3 query heads per kv head: a 16-row tile boundary falls inside a question."""
+    log(f"case: G=3 (Hq 6, Hkv 2) fused={fused}")
+    wl = W.custom_workload(wid=240, dtype="bf16", num_prompts=2, hq=6, hkv=2, head_dim=128,
+                           ctx_len=(90, 300), questions=(7, 13), seg_len=(2, 30), steps=2,
+                           value_std=0.5)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    for rows in (16, 32, 64):
+        gpu = run_gpu(st, [0, 1], [0, 1], kv=kv, fused=fused, tile_rows=rows, chunk_tokens=64)
+        ref = oracle_steps(st, kv, [0, 1], [0, 1])
+        assert gpu.err == 0
+        check(st, gpu, ref, [0, 1], f"G3-rows{rows}")
 
 
 def test_rope_base_500000_f32():
@@ -219,12 +265,15 @@ def test_llama3_8b_lc4096_n16_64_steps():
     kv = W.layer_kv(st)
     steps = list(range(64))
     rec = [0, 1, 32, 63]
-    gpu = run_gpu(st, steps, rec, kv=kv)
+    gpu = run_gpu(st, steps, rec, kv=kv, fused=True)
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec)
     check(st, gpu, ref, rec, "wl2")
-    std = run_gpu(st, [0], [0], standard=True, kv=kv)
+    assert counters_zero(gpu.batch)
+    std = run_gpu(st, [0], [0], standard=True, kv=kv, fused=True)
     check(st, std, {0: ref[0]}, [0], "wl2-standard")
+    sep = run_gpu(st, [0], [0], kv=kv, fused=False)
+    check(st, sep, {0: ref[0]}, [0], "wl2-separate")
 
 
 def test_ragged_b32_sampled():
@@ -235,7 +284,7 @@ def test_ragged_b32_sampled():
     rec = [0, 31]
     rng = np.random.default_rng(0)
     sel = {t: sorted(rng.choice(st.num_questions, 20, replace=False).tolist()) for t in rec}
-    gpu = run_gpu(st, steps, rec, kv=kv)
+    gpu = run_gpu(st, steps, rec, kv=kv, fused=True)
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec, questions=sel)
     check(st, gpu, ref, rec, "wl3", qsel=sel)
@@ -248,7 +297,7 @@ def test_long_context_sampled():
     steps = list(range(32))
     rec = [0, 31]
     sel = {0: [0, 17, 40, 63], 31: [5, 33, 62]}
-    gpu = run_gpu(st, steps, rec, kv=kv)
+    gpu = run_gpu(st, steps, rec, kv=kv, fused=True)
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec, questions=sel)
     check(st, gpu, ref, rec, "wl4", qsel=sel)
@@ -263,7 +312,7 @@ def test_32layer_sampled(layer):
     rec = [0, 15, 64, 127]
     rng = np.random.default_rng(layer)
     sel = {t: sorted(rng.choice(st.num_questions, 8, replace=False).tolist()) for t in rec}
-    gpu = run_gpu(st, steps, rec, layer=layer, kv=kv)
+    gpu = run_gpu(st, steps, rec, layer=layer, kv=kv, fused=True)
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec, layer=layer, questions=sel)
     check(st, gpu, ref, rec, f"wl5-L{layer}", qsel=sel)
