@@ -11,8 +11,8 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kTargetUnits = 1024;   // context units aimed for per launch (4 per CU)
-constexpr int kMinChunk = 128;
+constexpr int kTargetUnits = 512;    // context units aimed for per launch (2 resident per CU)
+constexpr int kMinChunk = 256;
 constexpr int kMaxChunk = 4096;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -60,14 +60,10 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   if (check_batch(bt) != IPPD_OK) return false;
   const int G = bt->num_q_heads / bt->num_kv_heads;
   const int64_t max_rows = shared ? static_cast<int64_t>(bt->max_questions) * G : G;
-  // rows per context unit: 16 -> four waves split the tokens of one 16-row
-  // block; 32/64/128 -> 2/4/8 waves each own a 16-row block of a shared tile
-  int rw = bt->tile_rows;
-  if (rw == 0) rw = max_rows <= 16 ? 16 : (max_rows <= 32 ? 32 : (max_rows <= 64 ? 64 : 128));
-  if (!shared) rw = 16;
-  const bool row_split = rw > 16;
-  const int waves = row_split ? rw / 16 : 4;
-  const int nrg = shared ? static_cast<int>((max_rows + rw - 1) / rw) : 1;
+  // waves per workgroup; a context unit covers 16 rows per wave
+  int waves = bt->tile_rows / 16;
+  if (waves == 0) waves = max_rows <= 16 ? 1 : (max_rows <= 32 ? 2 : (max_rows <= 64 ? 4 : 8));
+  const int nrg = static_cast<int>((max_rows + 16 * waves - 1) / (16 * waves));
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   int chunk = bt->chunk_tokens;
@@ -78,30 +74,25 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
     ch = ch < kMinChunk ? kMinChunk : (ch > kMaxChunk ? kMaxChunk : ch);
     chunk = static_cast<int>(ch);
   }
-  const int max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
-  const int64_t ctx_upg = static_cast<int64_t>(max_chunks) * nrg;
-  const int64_t seg_upg = shared ? (bt->max_questions + waves - 1) / waves : 1;
-  const int64_t upg = ctx_upg + seg_upg;
-  const int64_t gps = (n_groups + 7) / 8;
-  const int64_t per_slice = gps * upg;
-  if (per_slice * 8 > (1ll << 30) || n_groups == 0) return false;
+  const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
+  const int64_t seg_per_group = shared ? (bt->max_questions + waves - 1) / waves : 0;
+  const int64_t seg_units = shared ? n_groups * seg_per_group : (n_groups + waves - 1) / waves;
+  const int64_t seg_locals = (seg_units + 7) / 8;
+  const int64_t ctx_locals = nrg * ((n_groups * max_chunks + 7) / 8);
+  const int64_t grid = 8 * (seg_locals + ctx_locals);
+  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
-  pl->row_split = row_split ? 1 : 0;
-  pl->rw = rw;
   pl->nrg = nrg;
   pl->chunk = chunk;
-  pl->max_chunks = max_chunks;
-  pl->ctx_units_per_group = static_cast<int>(ctx_upg);
-  pl->seg_units_per_group = static_cast<int>(seg_upg);
-  pl->units_per_group = static_cast<int>(upg);
+  pl->max_chunks = static_cast<int>(max_chunks);
   pl->n_groups = static_cast<int>(n_groups);
-  pl->groups_per_slice = static_cast<int>(gps);
-  pl->per_slice = static_cast<int>(per_slice);
-  pl->grid = static_cast<int>(per_slice * 8);
+  pl->seg_per_group = static_cast<int>(seg_per_group);
+  pl->seg_units = static_cast<int>(seg_units);
+  pl->seg_locals = static_cast<int>(seg_locals);
+  pl->grid = static_cast<int>(grid);
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
-  pl->counters = static_cast<size_t>(n_groups) * seg_upg + bt->num_questions;
-  pl->off_acc = round256(pl->counters * sizeof(uint32_t));
+  pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(int32_t));
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
   return true;
@@ -145,22 +136,20 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.seg_len = bt->seg_len; p.active = bt->active; p.err_flag = bt->err_flag;
   p.out = out; p.lse = lse;
   char* ws = static_cast<char*>(workspace);
-  p.counters = reinterpret_cast<uint32_t*>(ws);
+  p.qmeta = reinterpret_cast<int32_t*>(ws);
   p.part_acc = reinterpret_cast<float*>(ws + pl.off_acc);
   p.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   p.pool = bt->ctx_pool_tokens;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hq = bt->num_q_heads; p.Hkv = bt->num_kv_heads;
   p.G = bt->num_q_heads / bt->num_kv_heads; p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
-  p.shared = pl.shared; p.fused = fused ? 1 : 0; p.rw = pl.rw; p.nrg = pl.nrg; p.chunk = pl.chunk;
-  p.max_chunks = pl.max_chunks;
-  p.ctx_units_per_group = pl.ctx_units_per_group; p.seg_units_per_group = pl.seg_units_per_group;
-  p.units_per_group = pl.units_per_group; p.n_groups = pl.n_groups;
-  p.groups_per_slice = pl.groups_per_slice; p.per_slice = pl.per_slice;
+  p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
+  p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.seg_per_group = pl.seg_per_group;
+  p.seg_units = pl.seg_units; p.seg_locals = pl.seg_locals;
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
-  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.row_split != 0, pl.grid, p, stream));
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.grid, p, stream));
 }
 
 }  // namespace
@@ -275,6 +264,6 @@ const char* ippd_status_string(ippd_status_t s) {
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 200; }
+int ippd_version(void) { return 300; }
 
 }  // extern "C"

@@ -37,27 +37,23 @@ struct AppendParams {
   double inv_freq[kMaxHalfDim];
 };
 
-// Launch plan of one decode-attention call.  Work is grouped per
-// (prompt, kv head) in IPPD mode and per (question, kv head) in the standard
-// baseline; a group owns its context units and its segment units, and the
-// groups are dealt in contiguous runs to the 8 workgroup slices (XCDs).
+// Launch plan of one decode call (attend_kernel + merge_kernel).  A group
+// is (prompt b, kv head g) for IPPD or (question i, kv head g) for the
+// standard baseline.  A context unit is (group, chunk, row group) with
+// 16*waves query rows; a segment unit holds `waves` segment tasks (one
+// (question, kv head) per wave).
 struct StepPlan {
   int shared;              // 1: IPPD, context units serve all active questions of a prompt
-  int waves;               // waves per workgroup (questions per segment unit in IPPD mode)
-  int row_split;           // 1: waves split a context unit's rows (16 each), 0: its tokens
-  int rw;                  // query rows per context unit
+  int waves;               // waves per workgroup
   int nrg;                 // row groups per group
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
-  int ctx_units_per_group; // max_chunks * nrg
-  int seg_units_per_group; // segment units (one question per wave) per group
-  int units_per_group;
   int n_groups;
-  int groups_per_slice;
-  int per_slice;
-  int grid;                // 8 * per_slice workgroups
+  int seg_per_group;       // IPPD: segment units per group
+  int seg_units;
+  int seg_locals;          // ceil(seg_units / 8): leading workgroups of every XCD slice
+  int grid;
   size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states
-  size_t counters;         // n_groups * seg_units_per_group + Nt 32-bit counters
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
   size_t workspace_bytes;
 };
@@ -70,13 +66,12 @@ struct StepParams {
   const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   float* out; float* lse;
-  uint32_t* counters;      // [n_groups * seg_units_per_group] arrivals, then [Nt] per-question
+  int32_t* qmeta;          // [Nt]: 1 + context chunks of a question served this call, else 0
   float* part_acc;         // [part_slots][D]
   float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
-  int shared, fused, rw, nrg, chunk, max_chunks;
-  int ctx_units_per_group, seg_units_per_group, units_per_group, n_groups, groups_per_slice, per_slice;
+  int shared, fused, nrg, chunk, max_chunks, n_groups, seg_per_group, seg_units, seg_locals;
   float c;                 // scale * log2(e)
   float scale;
   double inv_freq[kMaxHalfDim];
@@ -85,6 +80,6 @@ struct StepParams {
 hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s);
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
-hipError_t launch_step(int dtype, int waves, bool row_split, int grid, const StepParams& p, hipStream_t s);
+hipError_t launch_step(int dtype, int waves, int grid, const StepParams& p, hipStream_t s);
 
 }  // namespace ippd

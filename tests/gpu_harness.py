@@ -92,20 +92,11 @@ def oracle_steps(st: W.Structure, kv: W.LayerKV, steps: Iterable[int], record: S
     return res
 
 
-def counters_zero(db: DecodeBatch) -> bool:
-    """The arrival counters at the head of both workspaces are back at zero
-    (IPPD: B * Hkv * ceil(max_questions / 4) + Nt of them; baseline: Nt * Hkv + Nt)."""
+def bookkeeping_zero(db: DecodeBatch) -> bool:
+    """The per-question merge bookkeeping at the head of both workspaces (Nt
+    int32) is back at zero after every call."""
     torch.cuda.synchronize()
-    G = db.hq // db.hkv
-    rows = db.max_questions * G
-    tr = db.batches[0].tile_rows or (16 if rows <= 16 else 32 if rows <= 32 else 64 if rows <= 64 else 128)
-    waves = 4 if tr == 16 else tr // 16
-    n_ippd = db.B * db.hkv * ((db.max_questions + waves - 1) // waves) + db.Nt
-    n_std = db.Nt * db.hkv + db.Nt
-    ok = True
-    for ws, n in ((db.ws_ippd, n_ippd), (db.ws_std, n_std)):
-        ok &= bool(torch.all(ws[: 4 * n] == 0))
-    return ok
+    return bool(torch.all(db.ws_ippd[: 4 * db.Nt] == 0)) and bool(torch.all(db.ws_std[: 4 * db.Nt] == 0))
 
 
 def max_err(gpu: np.ndarray, ref: np.ndarray) -> float:

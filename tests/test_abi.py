@@ -125,17 +125,14 @@ def test_workspace_validation(lib):
 
 
 def test_workspace_formula(lib):
-    # counters (one per segment group of 4 questions per group, one per question), then
-    # (max_chunks + 1) * Nt * Hq partial states of D + 2 floats; each piece 256-byte rounded.
+    # one int per question (the merge bookkeeping), then (max_chunks + 1) * Nt * Hq
+    # partial states of D + 2 floats; each piece 256-byte rounded.  Both modes alike.
     bt = valid_batch(chunk_tokens=64)
     slots = (256 // 64 + 1) * 4 * 4
     r = lambda x: (x + 255) // 256 * 256
-    counters = 2 * 1 + 4            # B * Hkv groups x ceil(4 / 4) segment groups, + Nt
-    assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == \
-        r(counters * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
-    counters_std = 4 * 2 * 1 + 4    # Nt * Hkv groups x 1, + Nt
-    assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == \
-        r(counters_std * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
+    want = r(4 * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
+    assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == want
+    assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == want
 
 
 def test_step_pointer_validation(lib):
