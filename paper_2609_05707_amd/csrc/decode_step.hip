@@ -1,20 +1,19 @@
 // IPPD decode-step attention on gfx950: two launches per call.
 //
-//   attend_kernel  context units and segment tasks.  Each leaves, for every
-//                  query row it serves, an unnormalised partial softmax state
-//                  (running max, sum, weighted values) in the workspace.
-//   merge_kernel   one workgroup per question combines that question's
-//                  partial states exactly (splitting only regroups the sums
-//                  of attn_IPPD, Sec. 4.2), writes out/lse and, in the fused
-//                  step, advances the segment length.
+//   attend_kernel       context units: shared-context attention, one
+//                       unnormalised partial softmax state (running max,
+//                       sum, weighted values) per query row and chunk;
+//   segment_merge_kernel  one workgroup per (question, kv head): in the fused
+//                       step it rotates and appends the token fed this step,
+//                       attends over the question's own segment, and merges
+//                       that state exactly with the context chunks' (splitting
+//                       only regroups the sums of attn_IPPD, Sec. 4.2).
 // The launch boundary orders the two, so no unit ever waits for another.
 //
 // A *group* is (prompt b, kv head g) for IPPD or (question i, kv head g) for
-// the standard baseline.
-//
-// Context unit (group, chunk, row group): context tokens
-// [chunk*C, (chunk+1)*C) of prompt b against up to 16*NW query rows, the
-// (active question, head of group g) pairs.  IPPD serves all active
+// the standard baseline.  Context unit (group, chunk, row group): context
+// tokens [chunk*C, (chunk+1)*C) of prompt b against 16*NW query rows, the
+// (question, head of group g) pairs of the prompt in order.  IPPD serves all
 // questions of the prompt from one pass over the chunk, so K_c and V_c come
 // from HBM once for all M_j queries (Sec. 4.3); the baseline serves the G
 // rows of one question and reads the context once per question (App. A.2.2,
@@ -32,11 +31,10 @@
 // are XOR-swizzled in 16-byte chunks so that the 16 lanes of every ds_read
 // hit distinct bank groups of the 64-bank LDS.
 //
-// Segment task (question i, kv head g; one wave): the question's own
-// question+answer segment (M_qtn, Sec. 4.1).  In the fused step the wave
-// first rotates the step's key at virtual position ctx_len[b] + seg_len[i]
-// (Sec. 4.1) and appends key and value to the cache; its own attention takes
-// that token from registers, so it never waits for the store.
+// Segment (M_qtn, Sec. 4.1): four waves split the tiles of the question's
+// cached slots; its last key (the step's token, at virtual position
+// ctx_len[b] + seg_len[i]) is folded in from LDS, so the fused step never
+// waits for its own append.
 #include <float.h>
 
 #include "ippd_device.h"
@@ -125,27 +123,24 @@ __device__ __forceinline__ int tile_token(int kb, int lr) { return 8 * (lr >> 2)
 
 // ---------------------------------------------------------------------------
 // LDS ring of the context units.  A stage is one 32-token tile: K rows in
-// MFMA order (row r = 16*kb + lr), then the V^T rows (D rows of 32 tokens).
-// Both are stored in 16-byte chunks with chunk c of row r at position
-// c ^ swizzle(r).  A stage is filled by 1 KB DMA blocks: lane l of a block
-// writes bytes 16l..16l+15, so each lane fetches the global chunk that lands
-// at its position.
+// MFMA order (row r = 16*kb + lr), stored in 16-byte chunks with chunk c of
+// row r at position c ^ swizzle(r), then the tile's values exactly as cached
+// (four 8-token column blocks, contiguous).  A stage is filled by 1 KB DMA
+// blocks: lane l of a block writes bytes 16l..16l+15, so each lane fetches
+// the global chunk that lands at its position.
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, int NSTAGES>
 struct Ring {
   static constexpr int E = sizeof(T);
   static constexpr int KBYTES = 32 * D * E;
   static constexpr int STAGE = 2 * KBYTES;
-  static constexpr int NS = STAGE <= 16384 ? 4 : 2;     // stages (tiles in flight + 1)
+  static constexpr int NS = NSTAGES;                     // stages (tiles in flight + 1)
   static constexpr int BLOCKS = STAGE / 1024;
   static constexpr int KBLOCKS = KBYTES / 1024;
   static constexpr int CPR = D * E / 16;                 // chunks per key row
   static constexpr int KSH = CPR >= 16 ? 0 : 1;          // swizzle: bank groups distinct over
   static constexpr int KMASK = (CPR >= 16 ? 16 : CPR) - 1;   //   the 16 lanes of one read
-  static constexpr int VCPR = 2 * E;                     // chunks per V^T row (32 tokens)
-  static constexpr int VSH = VCPR == 4 ? 2 : 1;
-  static constexpr int VMASK = VCPR - 1;
-  static constexpr int TPC = 16 / E;                     // tokens per V^T chunk
+  static constexpr int VBLK = 8 * D * E;                 // bytes of one 8-token value block
   static_assert(64 % CPR == 0 || CPR == 64, "key rows must tile a 1 KB block");
 };
 
@@ -165,13 +160,13 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
 // Issue the DMA blocks of one tile (tokens [t0, t0+32) of [.., k1)) owned by
 // this wave: blocks wave, wave + NW, ...  Tokens past k1 are clamped to the
 // last valid one; the compute masks them.
-template <typename T, int D, int NW>
+template <typename T, int D, int NW, int NS>
 __device__ __forceinline__ void issue_tile(uint32_t stage, const T* __restrict__ kbase,
-                                           const T* __restrict__ vbase, int64_t pool, int64_t t0,
-                                           int64_t k1, int wave, int lane) {
-  using R = Ring<T, D>;
+                                           const T* __restrict__ vbase, int64_t t0, int64_t k1, int wave,
+                                           int lane) {
+  using R = Ring<T, D, NS>;
   constexpr int DPT = R::BLOCKS / NW;
-  const int64_t vlast = (k1 - 1) & ~static_cast<int64_t>(R::TPC - 1);
+  const int64_t vblk_last = (k1 - 1) >> 3;
 #pragma unroll
   for (int d = 0; d < DPT; ++d) {
     const int q = wave + NW * d;          // wave-uniform
@@ -183,11 +178,11 @@ __device__ __forceinline__ void issue_tile(uint32_t stage, const T* __restrict__
       tok = tok < k1 ? tok : k1 - 1;
       src = reinterpret_cast<const char*>(kbase + tok * D) + c * 16;
     } else {
-      const int dr = (q - R::KBLOCKS) * (64 / R::VCPR) + lane / R::VCPR;
-      const int c = (lane % R::VCPR) ^ ((dr >> R::VSH) & R::VMASK);
-      int64_t tok = t0 + c * R::TPC;
-      tok = tok < vlast ? tok : vlast;
-      src = vbase + static_cast<int64_t>(dr) * pool + tok;
+      const int o = (q - R::KBLOCKS) * 1024 + lane * 16;     // byte offset in the tile's values
+      const int jb = o / R::VBLK;
+      int64_t blk = (t0 >> 3) + jb;
+      blk = blk < vblk_last ? blk : vblk_last;
+      src = reinterpret_cast<const char*>(vbase + blk * 8 * D) + (o - jb * R::VBLK);
     }
     dma16(src, stage + static_cast<uint32_t>(q) * 1024u);
   }
@@ -249,10 +244,10 @@ __device__ __forceinline__ void mask_scores(f32x4_t (&sc)[2], int n, int lg) {
 
 // One ring tile for one 16-row block.  n = valid tokens of the tile (32 except
 // for the chunk's last tile).
-template <typename T, int D>
+template <typename T, int D, int NS>
 __device__ __forceinline__ void ring_tile(const unsigned char* stage, const typename Mfma<T>::Frag (&qf)[D / 32],
                                           RowState<D>& st, int n, int lr, int lg, float c) {
-  using R = Ring<T, D>;
+  using R = Ring<T, D, NS>;
   using M = Mfma<T>;
   constexpr int DS = D / 32;
   f32x4_t sc[2];
@@ -275,39 +270,22 @@ __device__ __forceinline__ void ring_tile(const unsigned char* stage, const type
   const int keep = min(max(n - 8 * lg, 0), 8);
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
-    const int d = 16 * db + lr;
-    const int sw = (d >> R::VSH) & R::VMASK;
-    const unsigned char* row = stage + R::KBYTES + d * (R::VCPR * 16);
-    const int c0 = 2 * lg * R::E / 4;                       // bf16: lg, fp32: 2*lg
-    typename M::Frag vf = M::lds2(row + ((c0 ^ sw) * 16), row + (((c0 + 1) ^ sw) * 16));
+    // block lg holds this lane's 8 tokens; dimension 16*db + lr of it
+    const unsigned char* vp = stage + R::KBYTES + lg * R::VBLK + (16 * db + lr) * 8 * R::E;
+    typename M::Frag vf = M::lds2(vp, vp + 16);
     if (n < 32) vf = M::keep_first(vf, keep);                // never NaN * 0 past the end
     st.o[db] = M::mma(vf, pf, st.o[db]);
   }
 }
 
-// Write one 16-row block's partial state to its slots (rows with valid).
+// Write one 16-row block's partial state to its slots.
 template <int D>
-__device__ __forceinline__ void publish_rows(const StepParams& p, const RowState<D>& st, int64_t slot,
-                                             bool valid, int lg) {
-  if (!valid) return;
+__device__ __forceinline__ void publish_rows(const StepParams& p, const RowState<D>& st, int64_t slot, int lg) {
   float* dst = p.part_acc + slot * D + 4 * lg;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) *reinterpret_cast<f32x4_t*>(dst + 16 * db) = st.o[db];
   if (lg == 0) *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(st.m, st.l);
 }
-
-// ---------------------------------------------------------------------------
-// Shared memory of attend_kernel.
-// ---------------------------------------------------------------------------
-template <typename T, int D, int NW>
-struct AttendSmem {
-  alignas(16) unsigned char ring[Ring<T, D>::NS * Ring<T, D>::STAGE];   // context units
-  alignas(16) T seg_k[NW][D];                 // segment tasks: the step's rotated key
-  alignas(16) T seg_v[NW][D];                 //   and value, per wave
-  int q[kMaxQuestionsPerPrompt];              // compacted active questions
-  int s[kMaxQuestionsPerPrompt];              // their segment lengths
-  int cnt[NW];
-};
 
 __device__ __forceinline__ bool prompt_layout_ok(const StepParams& p, int b) {
   const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
@@ -317,53 +295,87 @@ __device__ __forceinline__ bool prompt_layout_ok(const StepParams& p, int b) {
          off >= 0 && (off & 7) == 0 && len >= 0 && len <= p.max_ctx_len && off + len <= p.pool;
 }
 
-// Segment length a question's units work from; -1 if the question is skipped.
+// Segment length a question is served with; -1 if the question is skipped.
 __device__ __forceinline__ int usable_seg_len(const StepParams& p, int s) {
   if (p.fused) return (s >= 0 && s < p.seg_cap) ? s : -1;
   return (s >= 1 && s <= p.seg_cap) ? s : -1;
 }
 
-// Query fragments (B operand) of row `row` (question qi, head h): raw q_new
-// rotated at pos (fused step) or the given rotated queries.
+// Query fragments (B operand) of one row (question qi, head h), in two
+// steps so that all loads can be issued, and waited for, before the tile DMA
+// starts: fetch_q loads q_new (fused step; plus the rotation frequencies of
+// the lane's pairs) or the given rotated queries; rotate_q rotates q_new at
+// pos.  Lane (lg, lr) holds dims 32*ds + 8*lg + u; pair j (j < D/2) is
+// (x_j, x_{j+D/2}), i.e. fragment ds and ds + DS/2.
 template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void load_q(typename Mfma<T>::Frag (&qf)[D / 32], const StepParams& p, int qi, int h,
-                                       int64_t pos, int lg) {
+struct QFetch {
+  typename Mfma<T>::Frag f[D / 32];
+  double th[FUSED ? D / 8 : 1];
+};
+
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void fetch_q(QFetch<T, D, FUSED>& q, const StepParams& p, int qi, int h, int lg) {
   using M = Mfma<T>;
   constexpr int DS = D / 32;
-  if (FUSED) {
-    const T* qp = static_cast<const T*>(p.q_new) + (static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8;
-    f32x8_t x[DS];
+  const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8;
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) x[ds] = M::to_f32v(M::load(qp + 32 * ds));
+  for (int ds = 0; ds < DS; ++ds) q.f[ds] = M::load(src + 32 * ds);
+  if (FUSED) {
 #pragma unroll
     for (int ds = 0; ds < DS / 2; ++ds)
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        float cs, sn, xr, yr;
-        rope_cos_sin(pos, p.inv_freq[lg * 8 + 32 * ds + u], cs, sn);
-        rope_rotate(x[ds][u], x[ds + DS / 2][u], cs, sn, xr, yr);
-        x[ds][u] = xr;
-        x[ds + DS / 2][u] = yr;
-      }
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = M::from_f32(x[ds]);
-  } else {
-    const T* qp = static_cast<const T*>(p.q_rot_in) + (static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(qp + 32 * ds);
+      for (int u = 0; u < 8; ++u) q.th[8 * ds + u] = p.inv_freq[lg * 8 + 32 * ds + u];
   }
 }
 
-// ---------------------------------------------------------------------------
-// Context unit.
-// ---------------------------------------------------------------------------
-template <typename T, int D, int NW, bool FUSED>
-__device__ void context_unit(const StepParams& p, AttendSmem<T, D, NW>& sm, int grp, int chunk, int rg,
-                             int wave, int lane) {
-  using RG = Ring<T, D>;
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void rotate_q(typename Mfma<T>::Frag (&qf)[D / 32], const QFetch<T, D, FUSED>& q,
+                                         int64_t pos) {
   using M = Mfma<T>;
-  constexpr int NT = 64 * NW, RW = 16 * NW, DPT = RG::BLOCKS / NW;
-  const int tid = threadIdx.x, lr = lane & 15, lg = lane >> 4;
+  constexpr int DS = D / 32;
+  if (!FUSED) {
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[ds] = q.f[ds];
+    return;
+  }
+  f32x8_t x[DS];
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) x[ds] = M::to_f32v(q.f[ds]);
+#pragma unroll
+  for (int ds = 0; ds < DS / 2; ++ds)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      float cs, sn, xr, yr;
+      rope_cos_sin(pos, q.th[FUSED ? 8 * ds + u : 0], cs, sn);
+      rope_rotate(x[ds][u], x[ds + DS / 2][u], cs, sn, xr, yr);
+      x[ds][u] = xr;
+      x[ds + DS / 2][u] = yr;
+    }
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) qf[ds] = M::from_f32(x[ds]);
+}
+
+// ---------------------------------------------------------------------------
+// attend_kernel: context units.  blockIdx -> slice (XCD) = blockIdx & 7,
+// local = blockIdx >> 3; consecutive locals of a slice are the row groups of
+// one chunk (they share its tiles through that XCD's L2) and chunks are
+// dealt to the slices round robin.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int NW, int NS, bool FUSED>
+__global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
+  using RG = Ring<T, D, NS>;
+  using M = Mfma<T>;
+  constexpr int RW = 16 * NW, DPT = RG::BLOCKS / NW;
+  __shared__ __attribute__((aligned(16))) unsigned char ring[RG::NS * RG::STAGE];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int cl = local / p.nrg, rg = local - cl * p.nrg;
+  const int cglob = cl * 8 + slice;
+  if (cglob >= p.n_groups * p.max_chunks) return;
+  const int grp = cglob / p.max_chunks, chunk = cglob - grp * p.max_chunks;
+
   int b, g, qa, qb;
   if (p.shared) {
     g = grp / p.B;
@@ -374,57 +386,46 @@ __device__ void context_unit(const StepParams& p, AttendSmem<T, D, NW>& sm, int 
     b = prompt_of(p.q_start, p.B, qa);
   }
   if (!prompt_layout_ok(p, b)) {
-    if (tid == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
+    if (threadIdx.x == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
     return;
   }
   if (p.shared) { qa = p.q_start[b]; qb = p.q_start[b + 1]; } else { qb = qa + 1; }
+  const int G = p.G;
+  const int nrows = (qb - qa) * G;
+  const int row0 = rg * RW;
   const int ctx_len = p.ctx_len[b];
+  if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len || row0 >= nrows) return;
   const int64_t off = p.ctx_off[b];
-  if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len || qb == qa) return;
   const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
   const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
   const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
   const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
-  const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * D * p.pool;
-  const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sm.ring));
+  const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-  // the first NS-1 tiles go out before anything else
+  // this lane's row: question qa + row / G, head g*G + row % G.  Its loads
+  // all go out, and land, before the tile DMA: queued behind the DMA of
+  // every workgroup they would wait for all of it.
+  const int row = row0 + 16 * wave + lr;
+  const bool in_range = row < nrows;
+  const int rr = in_range ? row : nrows - 1;
+  const int qi = qa + rr / G, h = g * G + rr % G;
+  const bool a_raw = p.active[qi] != 0;
+  const int s_raw = FUSED ? p.seg_len[qi] : 0;
+  QFetch<T, D, FUSED> qraw;
+  fetch_q<T, D, FUSED>(qraw, p, qi, h, lg);
+  wait_vmcnt<0>();
+
+  // the first NS-1 tiles; the rotation below overlaps with them
 #pragma unroll
   for (int t = 0; t < RG::NS - 1; ++t)
-    issue_tile<T, D, NW>(ring + t * RG::STAGE, kbase, vbase, p.pool, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
+    issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
 
-  // rows: active questions of the group, compacted (with their segment lengths)
-  const int nq = qb - qa;
-  int n_act = 0;
-  for (int t0 = 0; t0 < nq; t0 += NT) {
-    const int t = t0 + tid;
-    const bool a = t < nq && p.active[qa + t];
-    const int s = t < nq ? p.seg_len[qa + t] : 0;
-    const unsigned long long ball = __ballot(a);
-    const int before = __popcll(ball & ((1ull << lane) - 1ull));
-    if (lane == 0) sm.cnt[wave] = __popcll(ball);
-    __syncthreads();
-    int wbase = n_act;
-    for (int w = 0; w < wave; ++w) wbase += sm.cnt[w];
-    if (a) { sm.q[wbase + before] = qa + t; sm.s[wbase + before] = s; }
-    for (int w = 0; w < NW; ++w) n_act += sm.cnt[w];
-    __syncthreads();
-  }
-  const int G = p.G;
-  const int nrows = n_act * G;
-  const int row0 = rg * RW;
-  if (row0 >= nrows) {
-    wait_vmcnt<0>();      // no LDS-DMA may outlive the workgroup
-    return;
-  }
-  const int rb0 = row0 + 16 * wave;
-  const bool live = rb0 < nrows;
-  const int row = rb0 + lr;
+  const bool act = in_range && a_raw;
+  const bool live = __any(act);                   // wave-uniform
   typename M::Frag qf[D / 32];
-  if (row < nrows) {
-    const int lq = row / G;
-    load_q<T, D, FUSED>(qf, p, sm.q[lq], g * G + row % G, static_cast<int64_t>(ctx_len) + sm.s[lq], lg);
-  } else {
+  rotate_q<T, D, FUSED>(qf, qraw, static_cast<int64_t>(ctx_len) + s_raw);
+  if (!act) {
 #pragma unroll
     for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
   }
@@ -437,297 +438,341 @@ __device__ void context_unit(const StepParams& p, AttendSmem<T, D, NW>& sm, int 
   const int last = ntiles - 1;
   const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
   for (int t = 0; t < ntiles; ++t) {
-    wait_vmcnt<(RG::NS - 2) * DPT>();
+    // tile t's blocks are this thread's oldest DMAs (at most 63 can be
+    // tracked: beyond that the wait is merely longer than needed)
+    wait_vmcnt<((RG::NS - 2) * DPT < 63 ? (RG::NS - 2) * DPT : 63)>();
     __syncthreads();
     const int tn = t + RG::NS - 1;
-    issue_tile<T, D, NW>(ring + (tn % RG::NS) * RG::STAGE, kbase, vbase, p.pool, k0 + 32ll * min(tn, last), k1,
-                         wave, lane);
-    if (live)
-      ring_tile<T, D>(sm.ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+    issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * min(tn, last), k1, wave,
+                             lane);
+    if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
   }
-  wait_vmcnt<0>();
+  wait_vmcnt<0>();                                // no LDS-DMA may outlive the workgroup
 
   float l = xor16_sum(st.l);
   st.l = xor32_sum(l);
-  if (live && row < nrows) {
-    const int lq = row / G;
-    const int64_t slot = (static_cast<int64_t>(chunk) * p.Nt + sm.q[lq]) * p.Hq + g * G + row % G;
-    publish_rows<D>(p, st, slot, true, lg);
-  }
+  if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
 }
 
 // ---------------------------------------------------------------------------
-// Segment task: question i (prompt b), kv head g, one wave.
+// segment_merge_kernel: workgroup (prompt b, question slot j, kv head g),
+// i.e. question i = q_start[b] + j, with kSegWaves waves.
 // ---------------------------------------------------------------------------
+constexpr int kSegWaves = 4;
+
 template <typename T, int D>
-struct SegTile {
-  typename Mfma<T>::Frag k[2][D / 32];
-  typename Mfma<T>::Frag v[D / 16];
+struct SegShared {
+  static constexpr int QROW = D * sizeof(T) + 16;   // padded: the 16 lanes of a read hit distinct banks
+  alignas(16) unsigned char q[16 * QROW];           // rotated queries of the G heads (rows >= G zero)
+  alignas(16) T k[D];                               // the last key and value
+  alignas(16) T v[D];
+  float m[kSegWaves][16], l[kSegWaves][16];
 };
 
-template <typename T, int D, int NW, bool FUSED>
-__device__ void segment_task(const StepParams& p, AttendSmem<T, D, NW>& sm, int i, int b, int g, int wave,
-                             int lane) {
+// Exact combination of partial softmax states (m, l, a) in 2^(c*x) units.
+struct MergeAcc {
+  float m, l;
+  f32x4_t a0, a1;
+  __device__ __forceinline__ void init() {
+    m = -INFINITY;
+    l = 0.f;
+    a0 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    a1 = a0;
+  }
+  __device__ __forceinline__ void fold(float mk, float lk, f32x4_t x0, f32x4_t x1, float c) {
+    const float mn = fmaxf(m, mk);
+    const float ms = mn == -INFINITY ? 0.f : mn;
+    const float sa = fast_exp2((m - ms) * c);        // 0 while m = -inf
+    const float sb = fast_exp2((mk - ms) * c);
+    l = l * sa + sb * lk;
+    a0 = a0 * sa + x0 * sb;
+    a1 = a1 * sa + x1 * sb;
+    m = mn;
+  }
+};
+
+template <typename T, int D, bool FUSED>
+__global__ __launch_bounds__(64 * kSegWaves) void segment_merge_kernel(StepParams p) {
   using M = Mfma<T>;
   using Frag = typename M::Frag;
+  using SS = SegShared<T, D>;
   constexpr int DS = D / 32, DB = D / 16;
+  __shared__ SS sh;
+  // dynamic: [kSegWaves][G][D] wave states, then [kSegWaves][G*D/8] merge partials
+  // (m, l, -, -, 8 values: 12 floats, the vectors 16-byte aligned)
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
   const int G = p.G;
+  const int g = blockIdx.x % p.Hkv;
+  const int jb = blockIdx.x / p.Hkv;
+  const int b = jb / p.max_questions, j = jb - b * p.max_questions;
+
+  // prompt metadata (one round trip), then the question's (a second)
+  if (!prompt_layout_ok(p, b)) {
+    if (tid == 0 && j == 0 && g == 0) raise_flag(p.err_flag, kFlagBadLayout);
+    return;
+  }
+  const int i = p.q_start[b] + j;
+  if (i >= p.q_start[b + 1]) return;
+  const int ctx_len = p.ctx_len[b];
+  const int nc = min((ctx_len + p.chunk - 1) / p.chunk, p.max_chunks);
+  if (!p.active[i]) return;
   const int sraw = p.seg_len[i];
   const int s = usable_seg_len(p, sraw);
   if (s < 0) {
-    if (lane == 0) {
-      raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
-      if (g == 0) p.qmeta[i] = 0;
-    }
+    if (tid == 0 && g == 0) raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
     return;
   }
-  const int ctx_len = p.ctx_len[b];
-  if (g == 0 && lane == 0) p.qmeta[i] = (ctx_len + p.chunk - 1) / p.chunk + 1;
   const int64_t sg = static_cast<int64_t>(i) * p.Hkv + g;
   T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
-  T* svp = static_cast<T*>(p.seg_vt) + sg * D * p.seg_cap;
-  Frag qf[DS];
-  int n_tok;                                   // keys attended: memory slots [0, s) (+ slot s)
+  T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
+  const int64_t pos = static_cast<int64_t>(ctx_len) + s;
+
+  // cached slots before the last key: wave w takes tiles w, w + 4, ...
+  const int mem = FUSED ? s : s - 1;
+  const int ntiles = (mem + 31) >> 5;
+  const int mlast = max(mem - 1, 0);
+  Frag kf[2][DS], vf[DB];
+  auto load_tile = [&](int t) {
+    const int t0 = 32 * t;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const T* kp = skp + static_cast<int64_t>(min(t0 + tile_token(kb, lr), mlast)) * D + lg * 8;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = M::load(kp + 32 * ds);
+    }
+    const T* vp = svp + static_cast<int64_t>(min((t0 >> 3) + lg, mlast >> 3)) * 8 * D + lr * 8;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) vf[db] = M::load(vp + 16 * db * 8);
+  };
+  if (wave < ntiles) load_tile(wave);
+
+  // queries of the G heads of group g (rotated at pos in the fused step) and
+  // the last key/value, into LDS
+  for (int e = tid; e < 16 * (D / 2); e += blockDim.x) {
+    const int r = e / (D / 2), jj = e - r * (D / 2);
+    T* qrow = reinterpret_cast<T*>(sh.q + r * SS::QROW);
+    if (r >= G) { qrow[jj] = from_f32<T>(0.f); qrow[jj + D / 2] = from_f32<T>(0.f); continue; }
+    const int64_t qo = (static_cast<int64_t>(i) * p.Hq + g * G + r) * D;
+    if (FUSED) {
+      const T* qn = static_cast<const T*>(p.q_new) + qo;
+      float cs, sn, x, y;
+      rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
+      rope_rotate(to_f32<T>(qn[jj]), to_f32<T>(qn[jj + D / 2]), cs, sn, x, y);
+      const T xq = from_f32<T>(x), yq = from_f32<T>(y);
+      qrow[jj] = xq;
+      qrow[jj + D / 2] = yq;
+      if (p.q_rot_out != nullptr) {
+        static_cast<T*>(p.q_rot_out)[qo + jj] = xq;
+        static_cast<T*>(p.q_rot_out)[qo + jj + D / 2] = yq;
+      }
+    } else {
+      const T* qr = static_cast<const T*>(p.q_rot_in) + qo;
+      qrow[jj] = qr[jj];
+      qrow[jj + D / 2] = qr[jj + D / 2];
+    }
+  }
   if (FUSED) {
-    // rotate and append this step's key/value at slot s, virtual position ctx_len + s
-    const int64_t pos = static_cast<int64_t>(ctx_len) + s;
+    // rotate and append this step's key/value at slot s (virtual position ctx_len + s)
     const T* kn = static_cast<const T*>(p.k_new) + sg * D;
     const T* vn = static_cast<const T*>(p.v_new) + sg * D;
-    for (int jj = lane; jj < D / 2; jj += 64) {
+    for (int jj = tid; jj < D / 2; jj += blockDim.x) {
       float cs, sn, x, y;
       rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
       rope_rotate(to_f32<T>(kn[jj]), to_f32<T>(kn[jj + D / 2]), cs, sn, x, y);
       const T xk = from_f32<T>(x), yk = from_f32<T>(y);
       skp[static_cast<int64_t>(s) * D + jj] = xk;
       skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
-      sm.seg_k[wave][jj] = xk;
-      sm.seg_k[wave][jj + D / 2] = yk;
+      sh.k[jj] = xk;
+      sh.k[jj + D / 2] = yk;
     }
-    for (int d = lane; d < D; d += 64) {
+    for (int d = tid; d < D; d += blockDim.x) {
       const T v = vn[d];
-      svp[static_cast<int64_t>(d) * p.seg_cap + s] = v;
-      sm.seg_v[wave][d] = v;
+      svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
+      sh.v[d] = v;
     }
-    // rotated queries of the G heads of group g (written out if asked)
-    if (lr < G) {
-      load_q<T, D, true>(qf, p, i, g * G + lr, pos, lg);
-      if (p.q_rot_out != nullptr) {
-        T* qo = static_cast<T*>(p.q_rot_out) + (static_cast<int64_t>(i) * p.Hq + g * G + lr) * D + lg * 8;
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) store8<T>(qo + 32 * ds, qf[ds]);
-      }
-    } else {
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) qf[ds] = M::zero();
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    n_tok = s + 1;
   } else {
-    if (lr < G) {
-      load_q<T, D, false>(qf, p, i, g * G + lr, 0, lg);
-    } else {
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) qf[ds] = M::zero();
+    for (int d = tid; d < D; d += blockDim.x) {
+      sh.k[d] = skp[static_cast<int64_t>(s - 1) * D + d];
+      sh.v[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
     }
-    n_tok = s;
   }
+  __syncthreads();
+
   RowState<D> st;
   row_init(st);
   const float c = p.c;
-  const int mem = FUSED ? s : n_tok;            // tokens read from the cache
-  const int ntiles = (n_tok + 31) >> 5;
-  const int mlast = max(mem - 1, 0);
-  const int vlast = mlast & ~7;
-  for (int t = 0; t < ntiles; ++t) {
-    const int t0 = 32 * t;
-    SegTile<T, D> tl;
+  const unsigned char* qrow = sh.q + lr * SS::QROW + lg * 8 * sizeof(T);
+  for (int t = wave; t < ntiles; t += kSegWaves) {
+    if (t != wave) load_tile(t);
+    const int n = min(mem - 32 * t, 32);
+    f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int tok = min(t0 + tile_token(kb, lr), mlast);
-      const T* kp = skp + static_cast<int64_t>(tok) * D + lg * 8;
+    for (int ds = 0; ds < DS; ++ds) {
+      const Frag qf = M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T)));
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) tl.k[kb][ds] = M::load(kp + 32 * ds);
-    }
-    {
-      const int tv = min(t0 + 8 * lg, vlast);
-      const T* vp = svp + static_cast<int64_t>(lr) * p.seg_cap + tv;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) tl.v[db] = M::load(vp + static_cast<int64_t>(16 * db) * p.seg_cap);
-    }
-    const int n = min(n_tok - t0, 32);
-    if (FUSED && t == ntiles - 1) {
-      // slot s (the step's token) comes from the wave's own copy
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        if (t0 + tile_token(kb, lr) == s) {
-#pragma unroll
-          for (int ds = 0; ds < DS; ++ds) tl.k[kb][ds] = M::load(&sm.seg_k[wave][32 * ds + lg * 8]);
-        }
-      const int e = s - t0 - 8 * lg;
-      if (e >= 0 && e < 8) {
-#pragma unroll
-        for (int db = 0; db < DB; ++db) tl.v[db] = M::put(tl.v[db], e, sm.seg_v[wave][16 * db + lr]);
-      }
-    }
-    f32x4_t sc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) acc = M::mma(tl.k[kb][ds], qf[ds], acc);
-      sc[kb] = acc;
+      for (int kb = 0; kb < 2; ++kb) sc[kb] = M::mma(kf[kb][ds], qf, sc[kb]);
     }
     if (n < 32) mask_scores(sc, n, lg);
     const Frag pf = softmax_step<T, D>(sc, st, c);
     const int keep = min(max(n - 8 * lg, 0), 8);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const Frag vf = n < 32 ? M::keep_first(tl.v[db], keep) : tl.v[db];
-      st.o[db] = M::mma(vf, pf, st.o[db]);
+      const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
+      st.o[db] = M::mma(v, pf, st.o[db]);
     }
   }
-  float l = xor16_sum(st.l);
-  st.l = xor32_sum(l);
-  const int64_t slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + i) * p.Hq + g * G + lr;
-  publish_rows<D>(p, st, slot, lr < G, lg);
-}
-
-// ---------------------------------------------------------------------------
-// attend_kernel: blockIdx -> slice (XCD) = blockIdx & 7, local = blockIdx >> 3.
-// The first seg_locals locals of every slice are segment units, then come
-// context units: consecutive locals of a slice are the row groups of one
-// chunk (they share its tiles through that XCD's L2), chunks are dealt to
-// the slices round robin.
-// ---------------------------------------------------------------------------
-template <typename T, int D, int NW, bool FUSED>
-__global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
-  __shared__ AttendSmem<T, D, NW> sm;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
-  if (local < p.seg_locals) {
-    const int u = local * 8 + slice;
-    if (u >= p.seg_units) return;
-    int i, b, g;
-    if (p.shared) {
-      const int grp = u / p.seg_per_group, j = u - grp * p.seg_per_group;
-      g = grp / p.B;
-      b = grp - g * p.B;
-      if (!prompt_layout_ok(p, b)) return;     // flagged by the group's context units
-      i = p.q_start[b] + NW * j + wave;
-      if (i >= p.q_start[b + 1]) return;
-    } else {
-      const int grp = u * NW + wave;
-      if (grp >= p.n_groups) return;
-      g = grp / p.Nt;
-      i = grp - g * p.Nt;
-      b = prompt_of(p.q_start, p.B, i);
-      if (!prompt_layout_ok(p, b)) return;
+  if (wave == 0) {
+    // the last key: score = q_row . k, folded in as one more token
+    float dot = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T))));
+      const f32x8_t kv = M::to_f32v(M::load(sh.k + 32 * ds + lg * 8));
+#pragma unroll
+      for (int u = 0; u < 8; ++u) dot = fmaf(qv[u], kv[u], dot);
     }
-    if (!p.active[i]) return;
-    segment_task<T, D, NW, FUSED>(p, sm, i, b, g, wave, lane);
-    return;
+    dot = xor16_sum(dot);
+    dot = xor32_sum(dot);
+    if (__any(dot > st.m)) {
+      const float mn = fmaxf(st.m, dot);
+      const float alpha = fast_exp2((st.m - mn) * c);
+      st.l *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) st.o[db] *= alpha;
+      st.m = mn;
+    }
+    const float pn = fast_exp2((dot - st.m) * c);
+    if (lg == 0) st.l += pn;                 // one lane per row: the sum is reduced over lg below
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) st.o[db][v] = fmaf(pn, to_f32<T>(sh.v[16 * db + 4 * lg + v]), st.o[db][v]);
   }
-  const int z = local - p.seg_locals;
-  const int cl = z / p.nrg, rg = z - cl * p.nrg;
-  const int cglob = cl * 8 + slice;
-  if (cglob >= p.n_groups * p.max_chunks) return;
-  const int grp = cglob / p.max_chunks, chunk = cglob - grp * p.max_chunks;
-  context_unit<T, D, NW, FUSED>(p, sm, grp, chunk, rg, wave, lane);
-}
-
-// ---------------------------------------------------------------------------
-// merge_kernel: workgroup per question; thread (head h, 8 dims) combines the
-// question's context chunks and its segment state:
-//   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void merge_kernel(StepParams p) {
-  __shared__ int s_meta;
-  const int i = blockIdx.x;
-  if (threadIdx.x == 0) {
-    // qmeta[i] = 1 + context chunks when this call's segment task of (i, head 0)
-    // ran; reset here so that a question no task reaches next call is skipped
-    const int meta = p.qmeta[i];
-    p.qmeta[i] = 0;
-    s_meta = p.active[i] ? meta : 0;
+  float* so = dyn;                                            // [kSegWaves][G][D]
+  float* mp = dyn + kSegWaves * G * D;                        // [kSegWaves][items][12]
+  {
+    float l = xor16_sum(st.l);
+    l = xor32_sum(l);
+    if (lg == 0) { sh.m[wave][lr] = st.m; sh.l[wave][lr] = l; }
+    if (lr < G) {
+      float* dst = so + (wave * G + lr) * D + 4 * lg;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4_t*>(dst + 16 * db) = st.o[db];
+    }
   }
   __syncthreads();
-  const int meta = s_meta;
-  if (meta <= 0) return;
-  const int nc = min(meta - 1, p.max_chunks);   // context chunks of the question's prompt
-  const int D = p.D;
-  const float c = p.c;
-  constexpr int kBatch = 8;
-  for (int e = threadIdx.x; e < p.Hq * D / 8; e += blockDim.x) {
-    const int h = (e * 8) / D, d0 = e * 8 - h * D;
-    float mx = -INFINITY, l = 0.f;
-    f32x4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 <= nc; k0 += kBatch) {
+
+  // merge.  Item (row r < G, dims d0..d0+7).  Wave w folds its own segment
+  // state and the context chunks k = w, w + 4, ... of every item, then one
+  // pass combines the four waves' results:
+  //   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l
+  const int items = G * (D / 8);
+  for (int e = lane; e < items; e += 64) {
+    const int r = e / (D / 8), d0 = (e - r * (D / 8)) * 8;
+    const int h = g * G + r;
+    MergeAcc acc;
+    acc.init();
+    constexpr int kBatch = 8;
+    for (int k0 = wave; k0 < nc; k0 += kSegWaves * kBatch) {
       float2 ml[kBatch];
       f32x4_t x0[kBatch], x1[kBatch];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int k = min(k0 + u, nc);
-        const int ck = k < nc ? k : p.max_chunks;
-        const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
+        const int k = min(k0 + kSegWaves * u, nc - 1);
+        const int64_t slot = (static_cast<int64_t>(k) * p.Nt + i) * p.Hq + h;
         ml[u] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
         const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
         x0[u] = src[0];
         x1[u] = src[1];
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const bool live = k0 + u <= nc;
-        const float mn = live ? fmaxf(mx, ml[u].x) : mx;
-        const float ms = mn == -INFINITY ? 0.f : mn;
-        const float sa = fast_exp2((mx - ms) * c);                        // 0 while mx = -inf
-        const float sb = live ? fast_exp2((ml[u].x - ms) * c) : 0.f;
-        l = l * sa + sb * ml[u].y;
-        a0 = a0 * sa + x0[u] * sb;
-        a1 = a1 * sa + x1[u] * sb;
-        mx = mn;
-      }
+      for (int u = 0; u < kBatch; ++u)
+        if (k0 + kSegWaves * u < nc) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
     }
-    const float inv = 1.f / l;
-    f32x4_t* dst = reinterpret_cast<f32x4_t*>(p.out + (static_cast<int64_t>(i) * p.Hq + h) * D + d0);
-    dst[0] = a0 * inv;
-    dst[1] = a1 * inv;
-    if (p.lse != nullptr && d0 == 0) p.lse[static_cast<int64_t>(i) * p.Hq + h] = mx * p.scale + logf(l);
+    {
+      const f32x4_t* src = reinterpret_cast<const f32x4_t*>(so + (wave * G + r) * D + d0);
+      acc.fold(sh.m[wave][r], sh.l[wave][r], src[0], src[1], c);
+    }
+    float* dst = mp + (wave * items + e) * 12;
+    dst[0] = acc.m;
+    dst[1] = acc.l;
+    *reinterpret_cast<f32x4_t*>(dst + 4) = acc.a0;
+    *reinterpret_cast<f32x4_t*>(dst + 8) = acc.a1;
   }
-  if (p.fused && threadIdx.x == 0) p.seg_len[i] = p.seg_len[i] + 1;
+  __syncthreads();
+  for (int e = tid; e < items; e += blockDim.x) {
+    const int r = e / (D / 8), d0 = (e - r * (D / 8)) * 8;
+    const int h = g * G + r;
+    MergeAcc acc;
+    acc.init();
+#pragma unroll
+    for (int w = 0; w < kSegWaves; ++w) {
+      const float* src = mp + (w * items + e) * 12;
+      acc.fold(src[0], src[1], *reinterpret_cast<const f32x4_t*>(src + 4), *reinterpret_cast<const f32x4_t*>(src + 8), c);
+    }
+    const float inv = 1.f / acc.l;
+    f32x4_t* dst = reinterpret_cast<f32x4_t*>(p.out + (static_cast<int64_t>(i) * p.Hq + h) * D + d0);
+    dst[0] = acc.a0 * inv;
+    dst[1] = acc.a1 * inv;
+    if (p.lse != nullptr && d0 == 0) p.lse[static_cast<int64_t>(i) * p.Hq + h] = acc.m * p.scale + logf(acc.l);
+  }
+  if (FUSED && tid == 0) {
+    // the last of question i's Hkv workgroups advances its segment: every one
+    // of them has read seg_len[i] before arriving
+    if (atomicAdd(p.counters + i, 1u) == static_cast<uint32_t>(p.Hkv - 1)) {
+      p.counters[i] = 0;
+      p.seg_len[i] = s + 1;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW>
+template <typename T, int D, int NW, int NS>
 static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
-  if (p.fused) attend_kernel<T, D, NW, true><<<grid, 64 * NW, 0, s>>>(p);
-  else attend_kernel<T, D, NW, false><<<grid, 64 * NW, 0, s>>>(p);
+  if (p.fused) attend_kernel<T, D, NW, NS, true><<<grid, 64 * NW, 0, s>>>(p);
+  else attend_kernel<T, D, NW, NS, false><<<grid, 64 * NW, 0, s>>>(p);
   return hipGetLastError();
+}
+
+// Ring depth: 4 stages (two workgroups per CU) in general; 8 (one per CU,
+// every tile of a short unit in flight at once) when the grid fits the chip
+// in one wave.  fp32 at D = 128 has 32 KB stages: 2 or 4.
+template <typename T, int D, int NW>
+static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStream_t s) {
+  constexpr int base = (2 * 32 * D * sizeof(T)) > 16384 ? 2 : 4;
+  return deep ? launch_attend<T, D, NW, 2 * base>(grid, p, s) : launch_attend<T, D, NW, base>(grid, p, s);
 }
 
 template <typename T, int D>
-static hipError_t launch_d(int waves, int grid, const StepParams& p, hipStream_t s) {
-  switch (waves) {
-    case 1: return launch_attend<T, D, 1>(grid, p, s);
-    case 2: return launch_attend<T, D, 2>(grid, p, s);
-    case 4: return launch_attend<T, D, 4>(grid, p, s);
-    default: return launch_attend<T, D, 8>(grid, p, s);
+static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  hipError_t e = hipSuccess;
+  if (grid > 0) {
+    switch (waves) {
+      case 1: e = launch_depth<T, D, 1>(deep, grid, p, s); break;
+      case 2: e = launch_depth<T, D, 2>(deep, grid, p, s); break;
+      case 4: e = launch_depth<T, D, 4>(deep, grid, p, s); break;
+      default: e = launch_depth<T, D, 8>(deep, grid, p, s); break;
+    }
+    if (e != hipSuccess) return e;
   }
+  // LDS: the waves' segment states, then their merge partials (12 floats per item)
+  const size_t dyn = static_cast<size_t>(kSegWaves) * p.G * D * sizeof(float) +
+                     static_cast<size_t>(kSegWaves) * p.G * (D / 8) * 12 * sizeof(float);
+  const unsigned nblk = static_cast<unsigned>(p.B) * p.max_questions * p.Hkv;
+  if (p.fused) segment_merge_kernel<T, D, true><<<nblk, 64 * kSegWaves, dyn, s>>>(p);
+  else segment_merge_kernel<T, D, false><<<nblk, 64 * kSegWaves, dyn, s>>>(p);
+  return hipGetLastError();
 }
 
-hipError_t launch_step(int dtype, int waves, int grid, const StepParams& p, hipStream_t s) {
-  if (grid <= 0) return hipSuccess;
-  hipError_t e;
+hipError_t launch_step(int dtype, int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  if (p.Nt == 0) return hipSuccess;
   if (dtype == 0)
-    e = p.D == 64 ? launch_d<float, 64>(waves, grid, p, s) : launch_d<float, 128>(waves, grid, p, s);
-  else
-    e = p.D == 64 ? launch_d<uint16_t, 64>(waves, grid, p, s) : launch_d<uint16_t, 128>(waves, grid, p, s);
-  if (e != hipSuccess) return e;
-  merge_kernel<<<p.Nt, 256, 0, s>>>(p);
-  return hipGetLastError();
+    return p.D == 64 ? launch_d<float, 64>(waves, deep, grid, p, s) : launch_d<float, 128>(waves, deep, grid, p, s);
+  return p.D == 64 ? launch_d<uint16_t, 64>(waves, deep, grid, p, s)
+                   : launch_d<uint16_t, 128>(waves, deep, grid, p, s);
 }
 
 }  // namespace ippd

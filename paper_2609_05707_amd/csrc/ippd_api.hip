@@ -47,6 +47,20 @@ float softmax_scale(const ippd_batch_t* bt) {
 
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Compute units of the current device (256 on MI355X); queried once.
+int compute_units() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
 // theta_j = base^(-2j/D) in fp64, the rotation frequencies of pair j.
 void fill_inv_freq(const ippd_batch_t* bt, double* out) {
   const int half = bt->head_dim / 2;
@@ -75,24 +89,20 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
     chunk = static_cast<int>(ch);
   }
   const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
-  const int64_t seg_per_group = shared ? (bt->max_questions + waves - 1) / waves : 0;
-  const int64_t seg_units = shared ? n_groups * seg_per_group : (n_groups + waves - 1) / waves;
-  const int64_t seg_locals = (seg_units + 7) / 8;
-  const int64_t ctx_locals = nrg * ((n_groups * max_chunks + 7) / 8);
-  const int64_t grid = 8 * (seg_locals + ctx_locals);
-  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
+  const int64_t grid = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
+  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) ||
+      static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads > (1ll << 31) - 1)
+    return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
   pl->nrg = nrg;
   pl->chunk = chunk;
   pl->max_chunks = static_cast<int>(max_chunks);
   pl->n_groups = static_cast<int>(n_groups);
-  pl->seg_per_group = static_cast<int>(seg_per_group);
-  pl->seg_units = static_cast<int>(seg_units);
-  pl->seg_locals = static_cast<int>(seg_locals);
   pl->grid = static_cast<int>(grid);
-  pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
-  pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(int32_t));
+  pl->deep = grid <= compute_units() ? 1 : 0;
+  pl->part_slots = static_cast<size_t>(max_chunks) * bt->num_questions * bt->num_q_heads;
+  pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(uint32_t));
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
   return true;
@@ -136,7 +146,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.seg_len = bt->seg_len; p.active = bt->active; p.err_flag = bt->err_flag;
   p.out = out; p.lse = lse;
   char* ws = static_cast<char*>(workspace);
-  p.qmeta = reinterpret_cast<int32_t*>(ws);
+  p.counters = reinterpret_cast<uint32_t*>(ws);
   p.part_acc = reinterpret_cast<float*>(ws + pl.off_acc);
   p.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   p.pool = bt->ctx_pool_tokens;
@@ -144,12 +154,11 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.G = bt->num_q_heads / bt->num_kv_heads; p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
   p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
-  p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.seg_per_group = pl.seg_per_group;
-  p.seg_units = pl.seg_units; p.seg_locals = pl.seg_locals;
+  p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups;
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
-  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.grid, p, stream));
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.deep != 0, pl.grid, p, stream));
 }
 
 }  // namespace

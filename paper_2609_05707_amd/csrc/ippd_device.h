@@ -35,15 +35,30 @@ template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f32_to_bf16(x); }
 
-// cos/sin of pos * theta.  The angle is formed and reduced to [-pi, pi] in
-// fp64 (2*pi split hi + lo), then evaluated with fp32 sincos: the result is
-// accurate to a few 1e-7 for any position, where an fp32 angle would be off
-// by ~pos * 6e-8 rad.
+// cos/sin of pos * theta.  The angle is formed in fp64 and reduced to
+// r in [-pi/4, pi/4] about the nearest multiple k*pi/2 (pi/2 split hi + lo),
+// so the reduction is exact to ~1e-16 for any position; sin r and cos r then
+// come from their Taylor series in fp32 (terms to r^9 and r^10: truncation
+// below 2e-9 on that interval) and k mod 4 picks and signs them.  Accurate to
+// about 1e-7 everywhere, where an fp32 angle would be off by ~pos * 6e-8 rad.
 __device__ __forceinline__ void rope_cos_sin(int64_t pos, double theta, float& c, float& s) {
   const double ang = static_cast<double>(pos) * theta;
-  const double k = rint(ang * 0.15915494309189535);
-  const double r = fma(-k, 6.283185307179586, ang) - k * 2.4492935982947064e-16;
-  sincosf(static_cast<float>(r), &s, &c);
+  const double k = rint(ang * 0.63661977236758134);                          // 2/pi
+  const double r = fma(-k, 1.5707963267948966, ang) - k * 6.123233995736766e-17;
+  const float x = static_cast<float>(r), x2 = x * x;
+  float sp = fmaf(x2, 2.75573192e-6f, -1.98412698e-4f);     //  1/9!, -1/7!
+  sp = fmaf(x2, sp, 8.33333333e-3f);                        //  1/5!
+  sp = fmaf(x2, sp, -1.66666667e-1f);                       // -1/3!
+  const float sn = fmaf(x * x2, sp, x);
+  float cp = fmaf(x2, -2.75573192e-7f, 2.48015873e-5f);     // -1/10!, 1/8!
+  cp = fmaf(x2, cp, -1.38888889e-3f);                       // -1/6!
+  cp = fmaf(x2, cp, 4.16666667e-2f);                        //  1/4!
+  cp = fmaf(x2, cp, -0.5f);                                 // -1/2!
+  const float cs = fmaf(x2, cp, 1.0f);
+  const int q = static_cast<int>(static_cast<int64_t>(k) & 3);   // angle = r + q*pi/2
+  const float c0 = (q & 1) ? sn : cs, s0 = (q & 1) ? cs : sn;
+  c = ((q + 1) & 2) ? -c0 : c0;                             // q = 1, 2: cos < 0 side
+  s = (q & 2) ? -s0 : s0;                                   // q = 2, 3: sin < 0 side
 }
 
 // Rotate one pair (a, b) = (x_j, x_{j+D/2}) by (c, s) = (cos, sin); written with
@@ -75,6 +90,15 @@ __device__ __forceinline__ float xor32_sum(float x) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Values are cached transposed in 8-token column blocks: for a region of n
+// tokens (n a multiple of 8), token t of dimension d sits at
+//   region * n * D + (t / 8) * 8 * D + d * 8 + t % 8,
+// so the 8 tokens of one dimension are 16 (bf16) or 32 (fp32) contiguous
+// bytes and a 32-token tile of all D dimensions is one contiguous block.
+__device__ __forceinline__ int64_t vt_index(int64_t region, int64_t n, int D, int64_t t, int d) {
+  return region * n * D + (t >> 3) * 8 * D + d * 8 + (t & 7);
+}
 
 // Prompt owning question i: the largest b with q_start[b] <= i (q_start has B+1 entries).
 __device__ __forceinline__ int prompt_of(const int32_t* q_start, int B, int i) {

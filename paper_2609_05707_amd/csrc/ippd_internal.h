@@ -37,23 +37,20 @@ struct AppendParams {
   double inv_freq[kMaxHalfDim];
 };
 
-// Launch plan of one decode call (attend_kernel + merge_kernel).  A group
-// is (prompt b, kv head g) for IPPD or (question i, kv head g) for the
-// standard baseline.  A context unit is (group, chunk, row group) with
-// 16*waves query rows; a segment unit holds `waves` segment tasks (one
-// (question, kv head) per wave).
+// Launch plan of one decode call (attend_kernel + segment_merge_kernel).  A
+// group is (prompt b, kv head g) for IPPD or (question i, kv head g) for the
+// standard baseline; a context unit is (group, chunk, row group) with
+// 16*waves query rows.
 struct StepPlan {
-  int shared;              // 1: IPPD, context units serve all active questions of a prompt
-  int waves;               // waves per workgroup
+  int shared;              // 1: IPPD, context units serve all questions of a prompt
+  int waves;               // waves per context unit
   int nrg;                 // row groups per group
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
   int n_groups;
-  int seg_per_group;       // IPPD: segment units per group
-  int seg_units;
-  int seg_locals;          // ceil(seg_units / 8): leading workgroups of every XCD slice
-  int grid;
-  size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states
+  int grid;                // attend_kernel workgroups
+  int deep;                // 1: deep LDS ring (grid fits the chip in one wave)
+  size_t part_slots;       // max_chunks * Nt * Hq partial softmax states
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
   size_t workspace_bytes;
 };
@@ -66,12 +63,12 @@ struct StepParams {
   const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   float* out; float* lse;
-  int32_t* qmeta;          // [Nt]: 1 + context chunks of a question served this call, else 0
+  uint32_t* counters;      // [Nt] per-question arrivals of the fused step (zero between calls)
   float* part_acc;         // [part_slots][D]
   float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
-  int shared, fused, nrg, chunk, max_chunks, n_groups, seg_per_group, seg_units, seg_locals;
+  int shared, fused, nrg, chunk, max_chunks, n_groups;
   float c;                 // scale * log2(e)
   float scale;
   double inv_freq[kMaxHalfDim];
@@ -80,6 +77,6 @@ struct StepParams {
 hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s);
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
-hipError_t launch_step(int dtype, int waves, int grid, const StepParams& p, hipStream_t s);
+hipError_t launch_step(int dtype, int waves, bool deep, int grid, const StepParams& p, hipStream_t s);
 
 }  // namespace ippd

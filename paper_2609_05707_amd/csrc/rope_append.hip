@@ -73,8 +73,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
   for (int e = threadIdx.x; e < p.Hkv * D; e += blockDim.x) {
     const int g = e / D, d = e - g * D;
     const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D + d;
-    const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * D + d) * p.seg_cap + s;
-    svt[dst] = vn[src];
+    svt[vt_index(static_cast<int64_t>(i) * p.Hkv + g, p.seg_cap, D, s, d)] = vn[src];
   }
   __syncthreads();   // every thread has read seg_len[i] before it moves
   if (threadIdx.x == 0) p.seg_len[i] = s + 1;
@@ -117,7 +116,7 @@ __global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, 
     ck[dst + j] = from_f32<T>(x);
     ck[dst + j + half] = from_f32<T>(y);
   }
-  // values: transpose a [tokens][D] tile into [D][tokens] through LDS
+  // values: transpose a [tokens][D] tile into 8-token column blocks through LDS
   for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
     const int tt = e / D, d = e - tt * D;
     s_v[tt][d] = vr[((off + t0 + tt) * p.Hkv + g) * D + d];
@@ -125,7 +124,7 @@ __global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, 
   __syncthreads();
   for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
     const int d = e / nt, tt = e - d * nt;
-    cvt[(static_cast<int64_t>(g) * D + d) * p.pool + off + t0 + tt] = s_v[tt][d];
+    cvt[vt_index(g, p.pool, D, off + t0 + tt, d)] = s_v[tt][d];
   }
 }
 
@@ -173,7 +172,7 @@ __global__ __launch_bounds__(256) void load_segments_kernel(LoadSegmentsParams p
   __syncthreads();
   for (int e = threadIdx.x; e < nt * D; e += blockDim.x) {
     const int d = e / nt, tt = e - d * nt;
-    svt[((static_cast<int64_t>(i) * p.Hkv + g) * D + d) * p.seg_cap + t0 + tt] = s_v[tt][d];
+    svt[vt_index(static_cast<int64_t>(i) * p.Hkv + g, p.seg_cap, D, t0 + tt, d)] = s_v[tt][d];
   }
 }
 

@@ -61,10 +61,12 @@ class DecodeBatch:
         self.seg_len = [torch.zeros(max(self.Nt, 1), dtype=torch.int32, device=dev) for _ in range(layers)]
         td = self.tdtype
         self.ctx_k = [torch.empty(hkv, self.pool, head_dim, dtype=td, device=dev) for _ in range(layers)]
-        self.ctx_vt = [torch.empty(hkv, head_dim, self.pool, dtype=td, device=dev) for _ in range(layers)]
+        # values transposed in 8-token column blocks (see include/ippd.h)
+        self.ctx_vt = [torch.empty(hkv, self.pool // 8, head_dim, 8, dtype=td, device=dev) for _ in range(layers)]
         nt = max(self.Nt, 1)
         self.seg_k = [torch.empty(nt, hkv, self.seg_cap, head_dim, dtype=td, device=dev) for _ in range(layers)]
-        self.seg_vt = [torch.empty(nt, hkv, head_dim, self.seg_cap, dtype=td, device=dev) for _ in range(layers)]
+        self.seg_vt = [torch.empty(nt, hkv, self.seg_cap // 8, head_dim, 8, dtype=td, device=dev)
+                       for _ in range(layers)]
         self.batches = []
         self.caches = []
         for layer in range(layers):
@@ -113,6 +115,17 @@ class DecodeBatch:
     def to_dev(self, x) -> torch.Tensor:
         t = x if isinstance(x, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(x))
         return t.to(self.device).to(self.tdtype).contiguous()
+
+    def ctx_values(self, layer: int) -> torch.Tensor:
+        """Context values of one layer as [Hkv][D][pool] (a copy; the cache holds
+        them in 8-token column blocks)."""
+        x = self.ctx_vt[layer]
+        return x.permute(0, 2, 1, 3).reshape(self.hkv, self.D, self.pool)
+
+    def seg_values(self, layer: int) -> torch.Tensor:
+        """Segment values of one layer as [Nt][Hkv][D][seg_capacity] (a copy)."""
+        x = self.seg_vt[layer]
+        return x.permute(0, 1, 3, 2, 4).reshape(x.shape[0], self.hkv, self.D, self.seg_cap)
 
     def err_flag(self) -> int:
         return int(self.d_err.item())

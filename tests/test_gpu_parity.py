@@ -49,7 +49,7 @@ def test_tiny_f32_full():
     np.testing.assert_allclose(gpu.q_rot[0], q_ref, atol=2e-6, rtol=0)
     db = gpu.batch
     seg_k = db.seg_k[0].float().cpu().numpy()
-    seg_vt = db.seg_vt[0].float().cpu().numpy()
+    seg_vt = db.seg_values(0).float().cpu().numpy()
     for i in range(st.num_questions):
         s = st.seg_len0[i]
         k_ref = O.rope(si.k_new[i], pos[i], wl.rope_base)
@@ -60,7 +60,7 @@ def test_tiny_f32_full():
     ck = db.ctx_k[0].float().cpu().numpy()
     k_ctx_ref = O.rope(kv.ctx_k.transpose(1, 0, 2), np.arange(256)[None, :], wl.rope_base)
     np.testing.assert_allclose(ck[:, :256], k_ctx_ref, atol=2e-6, rtol=0)
-    np.testing.assert_array_equal(db.ctx_vt[0].float().cpu().numpy()[:, :, :256],
+    np.testing.assert_array_equal(db.ctx_values(0).float().cpu().numpy()[:, :, :256],
                                   kv.ctx_v.transpose(1, 2, 0))
 
 
@@ -107,7 +107,7 @@ def test_fused_step_equals_separate_calls(dtype):
         np.testing.assert_array_equal(a.out[t][act], b.out[t][act])
         np.testing.assert_array_equal(a.q_rot[t][act], b.q_rot[t][act])
     ka, kb = a.batch.seg_k[0].float().cpu().numpy(), b.batch.seg_k[0].float().cpu().numpy()
-    va, vb = a.batch.seg_vt[0].float().cpu().numpy(), b.batch.seg_vt[0].float().cpu().numpy()
+    va, vb = a.batch.seg_values(0).float().cpu().numpy(), b.batch.seg_values(0).float().cpu().numpy()
     for i, n in enumerate(st.seg_len_at(3)):           # filled slots only
         np.testing.assert_array_equal(ka[i, :, :n], kb[i, :, :n])
         np.testing.assert_array_equal(va[i, :, :, :n], vb[i, :, :, :n])
