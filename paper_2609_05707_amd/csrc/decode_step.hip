@@ -356,20 +356,211 @@ __device__ __forceinline__ void rotate_q(typename Mfma<T>::Frag (&qf)[D / 32], c
 }
 
 // ---------------------------------------------------------------------------
-// attend_kernel: context units.  blockIdx -> slice (XCD) = blockIdx & 7,
-// local = blockIdx >> 3; consecutive locals of a slice are the row groups of
-// one chunk (they share its tiles through that XCD's L2) and chunks are
-// dealt to the slices round robin.
+// Segment task (question i of prompt b, kv head g; one wave), run by the
+// context units once their chunk is done.  Fused step: rotate the step's
+// key at virtual position ctx_len + seg_len[i] and append it with its value;
+// the task's own attention folds that key in from LDS after streaming the
+// cached slots, so it never waits for the store.  Attention-only calls fold
+// slot seg_len[i] - 1 the same way, so both give identical sums.
 // ---------------------------------------------------------------------------
+template <typename T, int D>
+struct SegScratch {
+  static constexpr int QROW = D * sizeof(T) + 16;   // padded: the 16 lanes of a read hit distinct banks
+  alignas(16) unsigned char q[16 * QROW];           // rotated queries of the G heads (rows >= G zero)
+  alignas(16) T k[D];                               // the last key and value
+  alignas(16) T v[D];
+};
+
+template <typename T, int D, bool FUSED>
+__device__ void segment_task(const StepParams& p, SegScratch<T, D>& ws, int i, int ctx_len, int g, int lane) {
+  using M = Mfma<T>;
+  using Frag = typename M::Frag;
+  using SS = SegScratch<T, D>;
+  constexpr int DS = D / 32, DB = D / 16;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int G = p.G;
+  const int sraw = p.seg_len[i];
+  const int s = usable_seg_len(p, sraw);
+  if (s < 0) {
+    if (lane == 0 && g == 0) raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
+    return;
+  }
+  const int64_t sg = static_cast<int64_t>(i) * p.Hkv + g;
+  T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
+  T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
+  const int64_t pos = static_cast<int64_t>(ctx_len) + s;
+  {
+    // query rows: lane (lg, lr) holds head g*G + lr, dims 32*ds + 8*lg + u
+    const int h = g * G + (lr < G ? lr : 0);
+    const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + h) * D + lg * 8;
+    Frag qf[DS];
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
+    if (FUSED) {
+      // rotate pairs (j, j + D/2), j = 32*ds + 8*lg + u, at pos
+#pragma unroll
+      for (int ds = 0; ds < DS / 2; ++ds) {
+        f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          float cs, sn, xr, yr;
+          rope_cos_sin(pos, p.inv_freq[lg * 8 + 32 * ds + u], cs, sn);
+          rope_rotate(x[u], y[u], cs, sn, xr, yr);
+          x[u] = xr;
+          y[u] = yr;
+        }
+        qf[ds] = M::from_f32(x);
+        qf[ds + DS / 2] = M::from_f32(y);
+      }
+    }
+    if (lr >= G) {
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) qf[ds] = M::zero();
+    } else if (FUSED && p.q_rot_out != nullptr) {
+      T* qo = static_cast<T*>(p.q_rot_out) + (static_cast<int64_t>(i) * p.Hq + h) * D + lg * 8;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) store8<T>(qo + 32 * ds, qf[ds]);
+    }
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) store8<T>(reinterpret_cast<T*>(ws.q + lr * SS::QROW) + 32 * ds + lg * 8, qf[ds]);
+  }
+  if (FUSED) {
+    const T* kn = static_cast<const T*>(p.k_new) + sg * D;
+    const T* vn = static_cast<const T*>(p.v_new) + sg * D;
+    for (int jj = lane; jj < D / 2; jj += 64) {
+      float cs, sn, x, y;
+      rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
+      rope_rotate(to_f32<T>(kn[jj]), to_f32<T>(kn[jj + D / 2]), cs, sn, x, y);
+      const T xk = from_f32<T>(x), yk = from_f32<T>(y);
+      skp[static_cast<int64_t>(s) * D + jj] = xk;
+      skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
+      ws.k[jj] = xk;
+      ws.k[jj + D / 2] = yk;
+    }
+    for (int d = lane; d < D; d += 64) {
+      const T v = vn[d];
+      svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
+      ws.v[d] = v;
+    }
+  } else {
+    for (int d = lane; d < D; d += 64) {
+      ws.k[d] = skp[static_cast<int64_t>(s - 1) * D + d];
+      ws.v[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+
+  RowState<D> st;
+  row_init(st);
+  const float c = p.c;
+  const unsigned char* qrow = ws.q + lr * SS::QROW + lg * 8 * sizeof(T);
+  const int mem = FUSED ? s : s - 1;            // cached slots before the last key
+  const int ntiles = (mem + 31) >> 5;
+  const int mlast = max(mem - 1, 0);
+  // the segment bases are wave-uniform: loads take them as scalar bases plus
+  // 32-bit lane offsets (a segment holds < 2^31 elements)
+  const T* __restrict__ kseg = skp;
+  const T* __restrict__ vseg = svp;
+  for (int t = 0; t < ntiles; ++t) {
+    const int t0 = 32 * t;
+    Frag kf[2][DS], vf[DB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const uint32_t ko = static_cast<uint32_t>(min(t0 + tile_token(kb, lr), mlast) * D + lg * 8);
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = M::load(kseg + (ko + 32 * ds));
+    }
+    const uint32_t vo = static_cast<uint32_t>(min((t0 >> 3) + lg, mlast >> 3) * 8 * D + lr * 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) vf[db] = M::load(vseg + (vo + 16 * db * 8));
+    const int n = min(mem - t0, 32);
+    f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const Frag qf = M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T)));
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sc[kb] = M::mma(kf[kb][ds], qf, sc[kb]);
+    }
+    if (n < 32) mask_scores(sc, n, lg);
+    const Frag pf = softmax_step<T, D>(sc, st, c);
+    const int keep = min(max(n - 8 * lg, 0), 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
+      st.o[db] = M::mma(v, pf, st.o[db]);
+    }
+  }
+  {
+    // the last key: score = q_row . k, folded in as one more token
+    float dot = 0.f;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T))));
+      const f32x8_t kv = M::to_f32v(M::load(ws.k + 32 * ds + lg * 8));
+#pragma unroll
+      for (int u = 0; u < 8; ++u) dot = fmaf(qv[u], kv[u], dot);
+    }
+    dot = xor16_sum(dot);
+    dot = xor32_sum(dot);
+    if (__any(dot > st.m)) {
+      const float mn = fmaxf(st.m, dot);
+      const float alpha = fast_exp2((st.m - mn) * c);
+      st.l *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) st.o[db] *= alpha;
+      st.m = mn;
+    }
+    const float pn = fast_exp2((dot - st.m) * c);
+    if (lg == 0) st.l += pn;                 // one lane per row: the sum is reduced over lg below
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) st.o[db][v] = fmaf(pn, to_f32<T>(ws.v[16 * db + 4 * lg + v]), st.o[db][v]);
+  }
+  float l = xor16_sum(st.l);
+  st.l = xor32_sum(l);
+  if (lr < G) publish_rows<D>(p, st, (static_cast<int64_t>(p.max_chunks) * p.Nt + i) * p.Hq + g * G + lr, lg);
+}
+
+// ---------------------------------------------------------------------------
+// attend_kernel.  The first ctx_blocks workgroups are context units:
+// blockIdx -> slice (XCD) = blockIdx & 7, local = blockIdx >> 3;
+// consecutive locals of a slice are the row groups of one chunk (they share
+// its tiles through that XCD's L2) and chunks are dealt to the slices round
+// robin.  The remaining workgroups are segment units, NW segment tasks each
+// (task (b, j, g): question slot j of prompt b, kv head g).  Workgroups are
+// dispatched in order, so segment units start as context units retire and
+// fill the tail of the context work.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int NW, int NS>
+union AttendShared {
+  alignas(16) unsigned char ring[NS * 2 * 32 * D * sizeof(T)];
+  SegScratch<T, D> seg[NW];
+};
+
 template <typename T, int D, int NW, int NS, bool FUSED>
 __global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
   constexpr int RW = 16 * NW, DPT = RG::BLOCKS / NW;
-  __shared__ __attribute__((aligned(16))) unsigned char ring[RG::NS * RG::STAGE];
+  __shared__ AttendShared<T, D, NW, NS> sh;
+  unsigned char* ring = sh.ring;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lr = lane & 15, lg = lane >> 4;
+  if (static_cast<int>(blockIdx.x) >= p.ctx_blocks) {
+    // segment unit: task (b, j, g) per wave
+    const int task = (static_cast<int>(blockIdx.x) - p.ctx_blocks) * NW + wave;
+    const int g = task % p.Hkv, bj = task / p.Hkv;
+    const int b = bj / p.max_questions, j = bj - b * p.max_questions;
+    if (b >= p.B || !prompt_layout_ok(p, b)) return;
+    const int i = p.q_start[b] + j;
+    if (i >= p.q_start[b + 1] || !p.active[i]) return;
+    segment_task<T, D, FUSED>(p, sh.seg[wave], i, p.ctx_len[b], g, lane);
+    return;
+  }
   const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int cl = local / p.nrg, rg = local - cl * p.nrg;
   const int cglob = cl * 8 + slice;
@@ -391,83 +582,81 @@ __global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
   }
   if (p.shared) { qa = p.q_start[b]; qb = p.q_start[b + 1]; } else { qb = qa + 1; }
   const int G = p.G;
-  const int nrows = (qb - qa) * G;
+  const int nq = qb - qa;
+  const int nrows = nq * G;
   const int row0 = rg * RW;
   const int ctx_len = p.ctx_len[b];
   if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len || row0 >= nrows) return;
-  const int64_t off = p.ctx_off[b];
-  const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
-  const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
-  const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
-  const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
-  const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
-  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
+  {
+    const int64_t off = p.ctx_off[b];
+    const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
+    const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
+    const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
+    const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
+    const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
+    const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-  // this lane's row: question qa + row / G, head g*G + row % G.  Its loads
-  // all go out, and land, before the tile DMA: queued behind the DMA of
-  // every workgroup they would wait for all of it.
-  const int row = row0 + 16 * wave + lr;
-  const bool in_range = row < nrows;
-  const int rr = in_range ? row : nrows - 1;
-  const int qi = qa + rr / G, h = g * G + rr % G;
-  const bool a_raw = p.active[qi] != 0;
-  const int s_raw = FUSED ? p.seg_len[qi] : 0;
-  QFetch<T, D, FUSED> qraw;
-  fetch_q<T, D, FUSED>(qraw, p, qi, h, lg);
-  wait_vmcnt<0>();
+    // this lane's row: question qa + row / G, head g*G + row % G.  Its loads
+    // all go out, and land, before the tile DMA: queued behind the DMA of
+    // every workgroup they would wait for all of it.
+    const int row = row0 + 16 * wave + lr;
+    const bool in_range = row < nrows;
+    const int rr = in_range ? row : nrows - 1;
+    const int qi = qa + rr / G, h = g * G + rr % G;
+    const bool a_raw = p.active[qi] != 0;
+    const int s_raw = FUSED ? p.seg_len[qi] : 0;
+    QFetch<T, D, FUSED> qraw;
+    fetch_q<T, D, FUSED>(qraw, p, qi, h, lg);
+    wait_vmcnt<0>();
 
-  // the first NS-1 tiles; the rotation below overlaps with them
+    // the first NS-1 tiles; the rotation below overlaps with them
 #pragma unroll
-  for (int t = 0; t < RG::NS - 1; ++t)
-    issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
+    for (int t = 0; t < RG::NS - 1; ++t)
+      issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
 
-  const bool act = in_range && a_raw;
-  const bool live = __any(act);                   // wave-uniform
-  typename M::Frag qf[D / 32];
-  rotate_q<T, D, FUSED>(qf, qraw, static_cast<int64_t>(ctx_len) + s_raw);
-  if (!act) {
+    const bool act = in_range && a_raw;
+    const bool live = __any(act);                   // wave-uniform
+    typename M::Frag qf[D / 32];
+    rotate_q<T, D, FUSED>(qf, qraw, static_cast<int64_t>(ctx_len) + s_raw);
+    if (!act) {
 #pragma unroll
-    for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
-  }
-  RowState<D> st;
-  row_init(st);
-  const float c = p.c;
+      for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
+    }
+    RowState<D> st;
+    row_init(st);
+    const float c = p.c;
 
-  // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
-  // is refilled with tile t + NS - 1
-  const int last = ntiles - 1;
-  const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
-  for (int t = 0; t < ntiles; ++t) {
-    // tile t's blocks are this thread's oldest DMAs (at most 63 can be
-    // tracked: beyond that the wait is merely longer than needed)
-    wait_vmcnt<((RG::NS - 2) * DPT < 63 ? (RG::NS - 2) * DPT : 63)>();
-    __syncthreads();
-    const int tn = t + RG::NS - 1;
-    issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * min(tn, last), k1, wave,
-                             lane);
-    if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
-  }
-  wait_vmcnt<0>();                                // no LDS-DMA may outlive the workgroup
+    // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
+    // is refilled with tile t + NS - 1
+    const int last = ntiles - 1;
+    const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
+    for (int t = 0; t < ntiles; ++t) {
+      // tile t's blocks are this thread's oldest DMAs (at most 63 can be
+      // tracked: beyond that the wait is merely longer than needed)
+      wait_vmcnt<((RG::NS - 2) * DPT < 63 ? (RG::NS - 2) * DPT : 63)>();
+      __syncthreads();
+      const int tn = t + RG::NS - 1;
+      issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * min(tn, last), k1,
+                               wave, lane);
+      if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+    }
+    wait_vmcnt<0>();                                // no LDS-DMA may outlive the workgroup
 
-  float l = xor16_sum(st.l);
-  st.l = xor32_sum(l);
-  if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
+    float l = xor16_sum(st.l);
+    st.l = xor32_sum(l);
+    if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
+  }
+
 }
 
 // ---------------------------------------------------------------------------
-// segment_merge_kernel: workgroup (prompt b, question slot j, kv head g),
-// i.e. question i = q_start[b] + j, with kSegWaves waves.
+// merge_kernel: workgroup (prompt b, question slot j, kv head g), i.e.
+// question i = q_start[b] + j, kMergeWaves waves.  Item (row r < G, dims
+// d0..d0+7): wave w folds the context chunks k = w, w + 4, ... (wave 0 also
+// the segment state), then one pass combines the four waves' states:
+//   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l
 // ---------------------------------------------------------------------------
-constexpr int kSegWaves = 4;
-
-template <typename T, int D>
-struct SegShared {
-  static constexpr int QROW = D * sizeof(T) + 16;   // padded: the 16 lanes of a read hit distinct banks
-  alignas(16) unsigned char q[16 * QROW];           // rotated queries of the G heads (rows >= G zero)
-  alignas(16) T k[D];                               // the last key and value
-  alignas(16) T v[D];
-  float m[kSegWaves][16], l[kSegWaves][16];
-};
+constexpr int kMergeWaves = 4;
 
 // Exact combination of partial softmax states (m, l, a) in 2^(c*x) units.
 struct MergeAcc {
@@ -491,198 +680,41 @@ struct MergeAcc {
   }
 };
 
-template <typename T, int D, bool FUSED>
-__global__ __launch_bounds__(64 * kSegWaves) void segment_merge_kernel(StepParams p) {
-  using M = Mfma<T>;
-  using Frag = typename M::Frag;
-  using SS = SegShared<T, D>;
-  constexpr int DS = D / 32, DB = D / 16;
-  __shared__ SS sh;
-  // dynamic: [kSegWaves][G][D] wave states, then [kSegWaves][G*D/8] merge partials
-  // (m, l, -, -, 8 values: 12 floats, the vectors 16-byte aligned)
-  extern __shared__ __attribute__((aligned(16))) float dyn[];
+template <int D>
+__global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(StepParams p) {
+  extern __shared__ __attribute__((aligned(16))) float mp[];   // [kMergeWaves][items][12]
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int lr = lane & 15, lg = lane >> 4;
   const int G = p.G;
   const int g = blockIdx.x % p.Hkv;
   const int jb = blockIdx.x / p.Hkv;
   const int b = jb / p.max_questions, j = jb - b * p.max_questions;
-
-  // prompt metadata (one round trip), then the question's (a second)
-  if (!prompt_layout_ok(p, b)) {
-    if (tid == 0 && j == 0 && g == 0) raise_flag(p.err_flag, kFlagBadLayout);
-    return;
-  }
+  if (!prompt_layout_ok(p, b)) return;             // flagged by the context units
   const int i = p.q_start[b] + j;
   if (i >= p.q_start[b + 1]) return;
-  const int ctx_len = p.ctx_len[b];
-  const int nc = min((ctx_len + p.chunk - 1) / p.chunk, p.max_chunks);
+  const int nc = min((p.ctx_len[b] + p.chunk - 1) / p.chunk, p.max_chunks);
   if (!p.active[i]) return;
-  const int sraw = p.seg_len[i];
-  const int s = usable_seg_len(p, sraw);
-  if (s < 0) {
-    if (tid == 0 && g == 0) raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
-    return;
-  }
-  const int64_t sg = static_cast<int64_t>(i) * p.Hkv + g;
-  T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
-  T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
-  const int64_t pos = static_cast<int64_t>(ctx_len) + s;
-
-  // cached slots before the last key: wave w takes tiles w, w + 4, ...
-  const int mem = FUSED ? s : s - 1;
-  const int ntiles = (mem + 31) >> 5;
-  const int mlast = max(mem - 1, 0);
-  Frag kf[2][DS], vf[DB];
-  auto load_tile = [&](int t) {
-    const int t0 = 32 * t;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const T* kp = skp + static_cast<int64_t>(min(t0 + tile_token(kb, lr), mlast)) * D + lg * 8;
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = M::load(kp + 32 * ds);
-    }
-    const T* vp = svp + static_cast<int64_t>(min((t0 >> 3) + lg, mlast >> 3)) * 8 * D + lr * 8;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) vf[db] = M::load(vp + 16 * db * 8);
-  };
-  if (wave < ntiles) load_tile(wave);
-
-  // queries of the G heads of group g (rotated at pos in the fused step) and
-  // the last key/value, into LDS
-  for (int e = tid; e < 16 * (D / 2); e += blockDim.x) {
-    const int r = e / (D / 2), jj = e - r * (D / 2);
-    T* qrow = reinterpret_cast<T*>(sh.q + r * SS::QROW);
-    if (r >= G) { qrow[jj] = from_f32<T>(0.f); qrow[jj + D / 2] = from_f32<T>(0.f); continue; }
-    const int64_t qo = (static_cast<int64_t>(i) * p.Hq + g * G + r) * D;
-    if (FUSED) {
-      const T* qn = static_cast<const T*>(p.q_new) + qo;
-      float cs, sn, x, y;
-      rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
-      rope_rotate(to_f32<T>(qn[jj]), to_f32<T>(qn[jj + D / 2]), cs, sn, x, y);
-      const T xq = from_f32<T>(x), yq = from_f32<T>(y);
-      qrow[jj] = xq;
-      qrow[jj + D / 2] = yq;
-      if (p.q_rot_out != nullptr) {
-        static_cast<T*>(p.q_rot_out)[qo + jj] = xq;
-        static_cast<T*>(p.q_rot_out)[qo + jj + D / 2] = yq;
-      }
-    } else {
-      const T* qr = static_cast<const T*>(p.q_rot_in) + qo;
-      qrow[jj] = qr[jj];
-      qrow[jj + D / 2] = qr[jj + D / 2];
-    }
-  }
-  if (FUSED) {
-    // rotate and append this step's key/value at slot s (virtual position ctx_len + s)
-    const T* kn = static_cast<const T*>(p.k_new) + sg * D;
-    const T* vn = static_cast<const T*>(p.v_new) + sg * D;
-    for (int jj = tid; jj < D / 2; jj += blockDim.x) {
-      float cs, sn, x, y;
-      rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
-      rope_rotate(to_f32<T>(kn[jj]), to_f32<T>(kn[jj + D / 2]), cs, sn, x, y);
-      const T xk = from_f32<T>(x), yk = from_f32<T>(y);
-      skp[static_cast<int64_t>(s) * D + jj] = xk;
-      skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
-      sh.k[jj] = xk;
-      sh.k[jj + D / 2] = yk;
-    }
-    for (int d = tid; d < D; d += blockDim.x) {
-      const T v = vn[d];
-      svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
-      sh.v[d] = v;
-    }
-  } else {
-    for (int d = tid; d < D; d += blockDim.x) {
-      sh.k[d] = skp[static_cast<int64_t>(s - 1) * D + d];
-      sh.v[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
-    }
-  }
-  __syncthreads();
-
-  RowState<D> st;
-  row_init(st);
+  const int s = usable_seg_len(p, p.seg_len[i]);
+  if (s < 0) return;                               // flagged by the segment task
   const float c = p.c;
-  const unsigned char* qrow = sh.q + lr * SS::QROW + lg * 8 * sizeof(T);
-  for (int t = wave; t < ntiles; t += kSegWaves) {
-    if (t != wave) load_tile(t);
-    const int n = min(mem - 32 * t, 32);
-    f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const Frag qf = M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T)));
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) sc[kb] = M::mma(kf[kb][ds], qf, sc[kb]);
-    }
-    if (n < 32) mask_scores(sc, n, lg);
-    const Frag pf = softmax_step<T, D>(sc, st, c);
-    const int keep = min(max(n - 8 * lg, 0), 8);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
-      st.o[db] = M::mma(v, pf, st.o[db]);
-    }
-  }
-  if (wave == 0) {
-    // the last key: score = q_row . k, folded in as one more token
-    float dot = 0.f;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T))));
-      const f32x8_t kv = M::to_f32v(M::load(sh.k + 32 * ds + lg * 8));
-#pragma unroll
-      for (int u = 0; u < 8; ++u) dot = fmaf(qv[u], kv[u], dot);
-    }
-    dot = xor16_sum(dot);
-    dot = xor32_sum(dot);
-    if (__any(dot > st.m)) {
-      const float mn = fmaxf(st.m, dot);
-      const float alpha = fast_exp2((st.m - mn) * c);
-      st.l *= alpha;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) st.o[db] *= alpha;
-      st.m = mn;
-    }
-    const float pn = fast_exp2((dot - st.m) * c);
-    if (lg == 0) st.l += pn;                 // one lane per row: the sum is reduced over lg below
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) st.o[db][v] = fmaf(pn, to_f32<T>(sh.v[16 * db + 4 * lg + v]), st.o[db][v]);
-  }
-  float* so = dyn;                                            // [kSegWaves][G][D]
-  float* mp = dyn + kSegWaves * G * D;                        // [kSegWaves][items][12]
-  {
-    float l = xor16_sum(st.l);
-    l = xor32_sum(l);
-    if (lg == 0) { sh.m[wave][lr] = st.m; sh.l[wave][lr] = l; }
-    if (lr < G) {
-      float* dst = so + (wave * G + lr) * D + 4 * lg;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4_t*>(dst + 16 * db) = st.o[db];
-    }
-  }
-  __syncthreads();
-
-  // merge.  Item (row r < G, dims d0..d0+7).  Wave w folds its own segment
-  // state and the context chunks k = w, w + 4, ... of every item, then one
-  // pass combines the four waves' results:
-  //   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l
   const int items = G * (D / 8);
+  // slots of wave w: context chunks w, w + 4, ..., and (wave 0) the segment
+  const int nslot = (nc > wave ? (nc - wave + kMergeWaves - 1) / kMergeWaves : 0) + (wave == 0 ? 1 : 0);
   for (int e = lane; e < items; e += 64) {
     const int r = e / (D / 8), d0 = (e - r * (D / 8)) * 8;
     const int h = g * G + r;
     MergeAcc acc;
     acc.init();
     constexpr int kBatch = 8;
-    for (int k0 = wave; k0 < nc; k0 += kSegWaves * kBatch) {
+    for (int u0 = 0; u0 < nslot; u0 += kBatch) {
       float2 ml[kBatch];
       f32x4_t x0[kBatch], x1[kBatch];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int k = min(k0 + kSegWaves * u, nc - 1);
-        const int64_t slot = (static_cast<int64_t>(k) * p.Nt + i) * p.Hq + h;
+        const int uu = min(u0 + u, nslot - 1);
+        const int k = wave + kMergeWaves * uu;
+        const int ck = k < nc ? k : p.max_chunks;     // past the chunks: the segment slot
+        const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
         ml[u] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
         const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
         x0[u] = src[0];
@@ -690,11 +722,7 @@ __global__ __launch_bounds__(64 * kSegWaves) void segment_merge_kernel(StepParam
       }
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
-        if (k0 + kSegWaves * u < nc) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
-    }
-    {
-      const f32x4_t* src = reinterpret_cast<const f32x4_t*>(so + (wave * G + r) * D + d0);
-      acc.fold(sh.m[wave][r], sh.l[wave][r], src[0], src[1], c);
+        if (u0 + u < nslot) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
     }
     float* dst = mp + (wave * items + e) * 12;
     dst[0] = acc.m;
@@ -709,7 +737,7 @@ __global__ __launch_bounds__(64 * kSegWaves) void segment_merge_kernel(StepParam
     MergeAcc acc;
     acc.init();
 #pragma unroll
-    for (int w = 0; w < kSegWaves; ++w) {
+    for (int w = 0; w < kMergeWaves; ++w) {
       const float* src = mp + (w * items + e) * 12;
       acc.fold(src[0], src[1], *reinterpret_cast<const f32x4_t*>(src + 4), *reinterpret_cast<const f32x4_t*>(src + 8), c);
     }
@@ -719,7 +747,7 @@ __global__ __launch_bounds__(64 * kSegWaves) void segment_merge_kernel(StepParam
     dst[1] = acc.a1 * inv;
     if (p.lse != nullptr && d0 == 0) p.lse[static_cast<int64_t>(i) * p.Hq + h] = acc.m * p.scale + logf(acc.l);
   }
-  if (FUSED && tid == 0) {
+  if (p.fused && tid == 0) {
     // the last of question i's Hkv workgroups advances its segment: every one
     // of them has read seg_len[i] before arriving
     if (atomicAdd(p.counters + i, 1u) == static_cast<uint32_t>(p.Hkv - 1)) {
@@ -758,12 +786,10 @@ static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, 
     }
     if (e != hipSuccess) return e;
   }
-  // LDS: the waves' segment states, then their merge partials (12 floats per item)
-  const size_t dyn = static_cast<size_t>(kSegWaves) * p.G * D * sizeof(float) +
-                     static_cast<size_t>(kSegWaves) * p.G * (D / 8) * 12 * sizeof(float);
+  // LDS of the merge: the waves' partial states, 12 floats per item
+  const size_t dyn = static_cast<size_t>(kMergeWaves) * p.G * (D / 8) * 12 * sizeof(float);
   const unsigned nblk = static_cast<unsigned>(p.B) * p.max_questions * p.Hkv;
-  if (p.fused) segment_merge_kernel<T, D, true><<<nblk, 64 * kSegWaves, dyn, s>>>(p);
-  else segment_merge_kernel<T, D, false><<<nblk, 64 * kSegWaves, dyn, s>>>(p);
+  merge_kernel<D><<<nblk, 64 * kMergeWaves, dyn, s>>>(p);
   return hipGetLastError();
 }
 

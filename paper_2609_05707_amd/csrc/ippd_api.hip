@@ -89,7 +89,9 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
     chunk = static_cast<int>(ch);
   }
   const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
-  const int64_t grid = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
+  const int64_t ctx_blocks = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
+  const int64_t seg_tasks = static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads;
+  const int64_t grid = ctx_blocks + (seg_tasks + waves - 1) / waves;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) ||
       static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads > (1ll << 31) - 1)
     return false;
@@ -100,8 +102,9 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->max_chunks = static_cast<int>(max_chunks);
   pl->n_groups = static_cast<int>(n_groups);
   pl->grid = static_cast<int>(grid);
-  pl->deep = grid <= compute_units() ? 1 : 0;
-  pl->part_slots = static_cast<size_t>(max_chunks) * bt->num_questions * bt->num_q_heads;
+  pl->ctx_blocks = static_cast<int>(ctx_blocks);
+  pl->deep = ctx_blocks <= compute_units() ? 1 : 0;
+  pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(uint32_t));
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
@@ -154,7 +157,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.G = bt->num_q_heads / bt->num_kv_heads; p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
   p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
-  p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups;
+  p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.ctx_blocks = pl.ctx_blocks;
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);

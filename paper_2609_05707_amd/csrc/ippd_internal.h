@@ -37,7 +37,7 @@ struct AppendParams {
   double inv_freq[kMaxHalfDim];
 };
 
-// Launch plan of one decode call (attend_kernel + segment_merge_kernel).  A
+// Launch plan of one decode call (attend_kernel + merge_kernel).  A
 // group is (prompt b, kv head g) for IPPD or (question i, kv head g) for the
 // standard baseline; a context unit is (group, chunk, row group) with
 // 16*waves query rows.
@@ -48,9 +48,10 @@ struct StepPlan {
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
   int n_groups;
-  int grid;                // attend_kernel workgroups
+  int grid;                // attend_kernel workgroups: context units, then segment units
+  int ctx_blocks;          // context units (8 * nrg * ceil(n_groups * max_chunks / 8))
   int deep;                // 1: deep LDS ring (grid fits the chip in one wave)
-  size_t part_slots;       // max_chunks * Nt * Hq partial softmax states
+  size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states (chunks, segment)
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
   size_t workspace_bytes;
 };
@@ -68,7 +69,7 @@ struct StepParams {
   float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
-  int shared, fused, nrg, chunk, max_chunks, n_groups;
+  int shared, fused, nrg, chunk, max_chunks, n_groups, ctx_blocks;
   float c;                 // scale * log2(e)
   float scale;
   double inv_freq[kMaxHalfDim];
