@@ -2,9 +2,9 @@
 """Benchmark of the IPPD decode-step hot path on one MI355X.
 
 A step is one decode step of the workload: for every emulated layer, one
-ippd_decode_step launch (virtual-position rotation + KV append, shared-context
-and own-segment attention, exact merge), queued back-to-back on one stream
-with all inputs resident in HBM.  Each layer has
+ippd_decode_step call (virtual-position rotation + KV append, shared-context
+and own-segment attention, exact merge; two kernel launches), queued
+back-to-back on one stream with all inputs resident in HBM.  Each layer has
 its own KV cache (same values, distinct buffers), so a step streams every
 layer's context from HBM rather than from the 256 MB Infinity Cache.
 
@@ -18,7 +18,6 @@ identical KV, and the fp64 oracle is timed on a bounded sample on the host.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -48,7 +47,7 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="emulated layers cycled per step")
     ap.add_argument("--no-standard", action="store_true", help="skip the standard baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
-    ap.add_argument("--cpu-sample", type=int, default=48, help="question-steps the oracle computes")
+    ap.add_argument("--cpu-sample", type=int, default=400, help="question-steps the oracle computes")
     ap.add_argument("--chunk", type=int, default=0, help="context tokens per unit (0 = library default)")
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per context unit (0 = library default)")
     return ap.parse_args()
@@ -94,14 +93,6 @@ def step_flops(st: W.Structure, t: int) -> int:
     return tot
 
 
-def kernel_source_hash() -> str:
-    h = hashlib.sha256()
-    for f in ("decode_step.hip", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
-        with open(os.path.join(ROOT, "paper_2609_05707_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def read_traffic(workload_id: int):
     """HBM traffic per attention launch from the committed rocprofv3 counter summary,
     only if it was taken on the current kernel sources."""
@@ -110,6 +101,7 @@ def read_traffic(workload_id: int):
         return None
     with open(path) as f:
         rec = json.load(f)
+    from paper_2609_05707_amd.traffic import kernel_source_hash
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")
@@ -229,8 +221,8 @@ def main():
         return e0.elapsed_time(e1) / 1e3
 
     def kernel_time(standard=False):
-        """Average duration of the decode-step launches, from HIP events around each
-        launch on the launching stream, over a second pass of the same timed steps."""
+        """Average duration of one decode-step call (its two launches), from HIP events
+        around each call on the launching stream, over a second pass of the same steps."""
         reset()
         run(args.warmup, standard)
         reset()
@@ -274,7 +266,7 @@ def main():
             "layers_cycled": layers,
             "chunk_tokens": args.chunk or "auto",
             "tile_rows": args.tile_rows or "auto",
-            "step": "per layer: one ippd_decode_step launch (append + attention + merge)",
+            "step": "per layer: one ippd_decode_step call (append + attention + merge, two launches)",
             "us_per_layer_step": round(t_ippd / (steps * layers) * 1e6, 3),
             "separate_calls_us_per_layer_step": round(t_sep / (steps * layers) * 1e6, 3),
         },
@@ -283,7 +275,7 @@ def main():
         "mfma_tflops": round(flops_total / t_ippd / 1e12, 2),
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode_step_kernel (ippd_decode_step)",
+            "kernel": "attend_kernel + merge_kernel (one ippd_decode_step call)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

@@ -101,11 +101,13 @@ typedef struct ippd_batch {
 
 /*
  * KV cache (device buffers of the batch dtype).  Keys are stored rotated at
- * their virtual positions, token-major; values are stored transposed
- * (dimension-major, tokens contiguous) so that both operands of the two
- * products stream with 16-byte loads.
- *   ctx_k  [Hkv][ctx_pool_tokens][D]      ctx_vt [Hkv][D][ctx_pool_tokens]
- *   seg_k  [Nt][Hkv][seg_capacity][D]     seg_vt [Nt][Hkv][D][seg_capacity]
+ * their virtual positions, token-major.  Values are stored transposed in
+ * 8-token column blocks: for a region of n tokens, token t of dimension d is
+ * element (t / 8) * 8 * D + d * 8 + t % 8, so one dimension's 8 tokens are
+ * one 16-byte (bf16) fragment of the value-times-probability product and a
+ * 32-token tile of all dimensions is one contiguous block.
+ *   ctx_k  [Hkv][ctx_pool_tokens][D]      ctx_vt [Hkv][ctx_pool_tokens / 8][D][8]
+ *   seg_k  [Nt][Hkv][seg_capacity][D]     seg_vt [Nt][Hkv][seg_capacity / 8][D][8]
  * All four must be 16-byte aligned.
  */
 typedef struct ippd_kv_cache {
@@ -156,15 +158,15 @@ ippd_status_t ippd_append_kv(const ippd_batch_t *batch, const void *q_new,
                              const ippd_kv_cache_t *kv, hipStream_t stream);
 
 /*
- * Workspace of the decode calls: device scratch holding arrival counters and
- * the partial softmax states of the context chunks and segments.
- * ippd_decode_workspace_bytes serves ippd_decode_attention and
- * ippd_decode_step, standard_decode_workspace_bytes the two standard_* calls
- * (sizes depend only on host-side fields; 0 means an invalid batch).
- * A workspace must be 256-byte aligned and ZERO-FILLED before its first use;
- * every call leaves its counters at zero again, so it can be reused by later
- * calls on the same stream without clearing.  Calls that run concurrently
- * need separate workspaces.
+ * Workspace of the decode calls: device scratch holding one arrival counter
+ * per question and the partial softmax states (max, sum, weighted values) of
+ * the context chunks and segments.  ippd_decode_workspace_bytes serves
+ * ippd_decode_attention and ippd_decode_step, standard_decode_workspace_bytes
+ * the two standard_* calls (sizes depend only on host-side fields; 0 means an
+ * invalid batch).  A workspace must be 256-byte aligned and ZERO-FILLED
+ * before its first use; every call leaves its counters at zero again, so it
+ * can be reused by later calls on the same stream without clearing.  Calls
+ * that run concurrently need separate workspaces.
  */
 size_t ippd_decode_workspace_bytes(const ippd_batch_t *batch);
 size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
@@ -182,8 +184,8 @@ size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
  * (optional, may be NULL).  out [Nt][Hq][D] and lse [Nt][Hq] are float32;
  * rows of inactive questions are not written.
  * workspace: >= ippd_decode_workspace_bytes(batch) bytes (see above).
- * One kernel launch: chunk partials are merged in-kernel by whichever work
- * unit of a question group finishes last.
+ * Two kernel launches: the first computes one partial softmax state per
+ * (context chunk, row) and per (segment, row); the second merges them.
  */
 ippd_status_t ippd_decode_attention(const ippd_batch_t *batch, const void *q_rot,
                                     const ippd_kv_cache_t *kv, float *out, float *lse,
@@ -205,7 +207,7 @@ ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q
 
 /*
  * Fused decode step: ippd_append_kv followed by ippd_decode_attention, in
- * ONE kernel launch.  q_new [Nt][Hq][D], k_new/v_new [Nt][Hkv][D] are the
+ * the same two kernel launches as ippd_decode_attention.  q_new [Nt][Hq][D], k_new/v_new [Nt][Hkv][D] are the
  * raw (pre-rotation) projections of the token each active question feeds
  * this step.  The launch rotates them at virtual position
  * ctx_len[b] + seg_len[i], appends the key/value to the segment, attends

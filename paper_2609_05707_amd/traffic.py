@@ -1,0 +1,80 @@
+"""Turn rocprofv3 FETCH_SIZE / WRITE_SIZE counter runs into HBM bytes per call.
+
+Inputs are the ``*_counter_collection.csv`` files of four runs: the bench
+command and the calibration copy (``hbm_copy``), each once with FETCH_SIZE
+and once with WRITE_SIZE.  The copy moves a known number of bytes per
+dispatch in each direction, which fixes the counter scale; the decode
+kernels' per-dispatch counters are scaled by it and summed over the two
+launches of one decode call (attend_kernel + merge_kernel of the IPPD path).
+
+Usage: python -m paper_2609_05707_amd.traffic --fetch F.csv --write W.csv
+           --copy-fetch CF.csv --copy-write CW.csv --copy-mib 256
+           --workload 2 --command "..." --out profiles/traffic_decode_step_wl2.json
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+from collections import defaultdict
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("decode_step.hip", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
+        with open(os.path.join(ROOT, "paper_2609_05707_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def per_dispatch(path: str, counter: str):
+    """Mean counter value per dispatch, by kernel name prefix."""
+    vals = defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = "attend" if "attend_kernel" in name and "true>" in name else \
+                  "merge" if "merge_kernel" in name else \
+                  "copy" if "copyBuffer" in name else name
+            vals[key].append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in vals.items()}
+
+
+def main() -> None:
+    ap = argparse.ArgumentParser(description=__doc__)
+    for a in ("--fetch", "--write", "--copy-fetch", "--copy-write", "--command", "--out"):
+        ap.add_argument(a, required=True)
+    ap.add_argument("--copy-mib", type=int, default=256)
+    ap.add_argument("--workload", type=int, required=True)
+    args = ap.parse_args()
+    nbytes = args.copy_mib << 20
+    cf = per_dispatch(args.copy_fetch, "FETCH_SIZE").get("copy")
+    cw = per_dispatch(args.copy_write, "WRITE_SIZE").get("copy")
+    f = per_dispatch(args.fetch, "FETCH_SIZE")
+    w = per_dispatch(args.write, "WRITE_SIZE")
+    fs, ws = nbytes / cf, nbytes / cw
+    rec = {
+        "workload": args.workload,
+        "kernel_source_hash": kernel_source_hash(),
+        "command": args.command,
+        "copy_calibration": {"mib": args.copy_mib, "fetch_counter_per_dispatch": cf,
+                             "write_counter_per_dispatch": cw,
+                             "bytes_per_fetch_unit": fs, "bytes_per_write_unit": ws},
+        "attend_fetch_bytes": f.get("attend", 0.0) * fs, "attend_write_bytes": w.get("attend", 0.0) * ws,
+        "merge_fetch_bytes": f.get("merge", 0.0) * fs, "merge_write_bytes": w.get("merge", 0.0) * ws,
+    }
+    rec["hbm_bytes_per_launch"] = int(rec["attend_fetch_bytes"] + rec["attend_write_bytes"] +
+                                      rec["merge_fetch_bytes"] + rec["merge_write_bytes"])
+    with open(args.out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+if __name__ == "__main__":
+    main()
