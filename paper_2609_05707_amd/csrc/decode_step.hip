@@ -650,13 +650,17 @@ __global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// merge_kernel: workgroup (prompt b, question slot j, kv head g), i.e.
-// question i = q_start[b] + j, kMergeWaves waves.  Item (row r < G, dims
-// d0..d0+7): wave w folds the context chunks k = w, w + 4, ... (wave 0 also
-// the segment state), then one pass combines the four waves' states:
-//   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l
+// merge_kernel: question i = q_start[b] + j is served by merge_parts
+// workgroups of kMergeThreads threads.  Item (head h, dims d0..d0+7) of the
+// question combines its context chunks and its segment state:
+//   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l.
+// With P = merge_phases, a workgroup takes kMergeThreads / P items and P
+// threads per item, thread phase f folding slots f, f + P, ...; the P states
+// of an item are then combined through LDS.  The partial states are requested
+// together with the question's active flag and segment length.
 // ---------------------------------------------------------------------------
-constexpr int kMergeWaves = 4;
+constexpr int kMergeThreads = 512;
+constexpr int kMergeBatch = 8;       // partial states in flight per thread
 
 // Exact combination of partial softmax states (m, l, a) in 2^(c*x) units.
 struct MergeAcc {
@@ -681,78 +685,76 @@ struct MergeAcc {
 };
 
 template <int D>
-__global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(StepParams p) {
-  extern __shared__ __attribute__((aligned(16))) float mp[];   // [kMergeWaves][items][12]
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int G = p.G;
-  const int g = blockIdx.x % p.Hkv;
-  const int jb = blockIdx.x / p.Hkv;
-  const int b = jb / p.max_questions, j = jb - b * p.max_questions;
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
+  __shared__ __attribute__((aligned(16))) float mp[kMergeThreads * 12];   // (m, l, -, -, 8 values) per thread
+  const int tid = threadIdx.x;
+  const int P = p.merge_phases, per = kMergeThreads / P;
+  const int part = blockIdx.x % p.merge_parts, bj = blockIdx.x / p.merge_parts;
+  const int b = bj / p.max_questions, j = bj - b * p.max_questions;
   if (!prompt_layout_ok(p, b)) return;             // flagged by the context units
   const int i = p.q_start[b] + j;
   if (i >= p.q_start[b + 1]) return;
   const int nc = min((p.ctx_len[b] + p.chunk - 1) / p.chunk, p.max_chunks);
-  if (!p.active[i]) return;
-  const int s = usable_seg_len(p, p.seg_len[i]);
-  if (s < 0) return;                               // flagged by the segment task
+  const int nslot = nc + 1;                        // chunks, then the segment
   const float c = p.c;
-  const int items = G * (D / 8);
-  // slots of wave w: context chunks w, w + 4, ..., and (wave 0) the segment
-  const int nslot = (nc > wave ? (nc - wave + kMergeWaves - 1) / kMergeWaves : 0) + (wave == 0 ? 1 : 0);
-  for (int e = lane; e < items; e += 64) {
-    const int r = e / (D / 8), d0 = (e - r * (D / 8)) * 8;
-    const int h = g * G + r;
-    MergeAcc acc;
-    acc.init();
-    constexpr int kBatch = 8;
-    for (int u0 = 0; u0 < nslot; u0 += kBatch) {
-      float2 ml[kBatch];
-      f32x4_t x0[kBatch], x1[kBatch];
+  const int items = p.Hq * (D / 8);
+  const bool act = p.active[i] != 0;
+  const int s = usable_seg_len(p, p.seg_len[i]);
+  const int f = tid / per, local = tid - f * per;
+  const int e = part * per + local;                // this thread's item
+  const bool has = e < items;
+  const int h = has ? e / (D / 8) : 0, d0 = has ? (e - h * (D / 8)) * 8 : 0;
+  MergeAcc acc;
+  acc.init();
+  for (int k0 = f; k0 < nslot; k0 += P * kMergeBatch) {
+    float2 ml[kMergeBatch];
+    f32x4_t x0[kMergeBatch], x1[kMergeBatch];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int uu = min(u0 + u, nslot - 1);
-        const int k = wave + kMergeWaves * uu;
-        const int ck = k < nc ? k : p.max_chunks;     // past the chunks: the segment slot
-        const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
-        ml[u] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
-        const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
-        x0[u] = src[0];
-        x1[u] = src[1];
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u)
-        if (u0 + u < nslot) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const int k = min(k0 + P * u, nslot - 1);
+      const int ck = k < nc ? k : p.max_chunks;
+      const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
+      ml[u] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
+      const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
+      x0[u] = src[0];
+      x1[u] = src[1];
     }
-    float* dst = mp + (wave * items + e) * 12;
+    if (!act || s < 0) break;                      // inactive or skipped: nothing to write
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u)
+      if (k0 + P * u < nslot) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
+  }
+  if (!act || s < 0) return;                       // workgroup-uniform
+  if (P > 1) {
+    float* dst = mp + tid * 12;
     dst[0] = acc.m;
     dst[1] = acc.l;
     *reinterpret_cast<f32x4_t*>(dst + 4) = acc.a0;
     *reinterpret_cast<f32x4_t*>(dst + 8) = acc.a1;
-  }
-  __syncthreads();
-  for (int e = tid; e < items; e += blockDim.x) {
-    const int r = e / (D / 8), d0 = (e - r * (D / 8)) * 8;
-    const int h = g * G + r;
-    MergeAcc acc;
-    acc.init();
-#pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) {
-      const float* src = mp + (w * items + e) * 12;
-      acc.fold(src[0], src[1], *reinterpret_cast<const f32x4_t*>(src + 4), *reinterpret_cast<const f32x4_t*>(src + 8), c);
+    __syncthreads();
+    if (f == 0) {
+      for (int g2 = 1; g2 < P; ++g2) {
+        const float* src = mp + (g2 * per + local) * 12;
+        acc.fold(src[0], src[1], *reinterpret_cast<const f32x4_t*>(src + 4), *reinterpret_cast<const f32x4_t*>(src + 8), c);
+      }
     }
+  }
+  if (f == 0 && has) {
     const float inv = 1.f / acc.l;
     f32x4_t* dst = reinterpret_cast<f32x4_t*>(p.out + (static_cast<int64_t>(i) * p.Hq + h) * D + d0);
     dst[0] = acc.a0 * inv;
     dst[1] = acc.a1 * inv;
     if (p.lse != nullptr && d0 == 0) p.lse[static_cast<int64_t>(i) * p.Hq + h] = acc.m * p.scale + logf(acc.l);
   }
-  if (p.fused && tid == 0) {
-    // the last of question i's Hkv workgroups advances its segment: every one
-    // of them has read seg_len[i] before arriving
-    if (atomicAdd(p.counters + i, 1u) == static_cast<uint32_t>(p.Hkv - 1)) {
-      p.counters[i] = 0;
-      p.seg_len[i] = s + 1;
+  if (p.fused) {
+    // every thread of the workgroup has read seg_len[i] above; with several
+    // workgroups per question the last one to arrive advances it
+    __syncthreads();
+    if (tid == 0) {
+      if (p.merge_parts == 1 || atomicAdd(p.counters + i, 1u) == static_cast<uint32_t>(p.merge_parts - 1)) {
+        if (p.merge_parts > 1) p.counters[i] = 0;
+        p.seg_len[i] = s + 1;
+      }
     }
   }
 }
@@ -786,10 +788,8 @@ static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, 
     }
     if (e != hipSuccess) return e;
   }
-  // LDS of the merge: the waves' partial states, 12 floats per item
-  const size_t dyn = static_cast<size_t>(kMergeWaves) * p.G * (D / 8) * 12 * sizeof(float);
-  const unsigned nblk = static_cast<unsigned>(p.B) * p.max_questions * p.Hkv;
-  merge_kernel<D><<<nblk, 64 * kMergeWaves, dyn, s>>>(p);
+  const unsigned nblk = static_cast<unsigned>(p.B) * p.max_questions * p.merge_parts;
+  merge_kernel<D><<<nblk, kMergeThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -93,7 +93,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   const int64_t seg_tasks = static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads;
   const int64_t grid = ctx_blocks + (seg_tasks + waves - 1) / waves;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) ||
-      static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads > (1ll << 31) - 1)
+      static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads * 8 > (1ll << 31) - 1)
     return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
@@ -158,6 +158,16 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
   p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
   p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.ctx_blocks = pl.ctx_blocks;
+  // merge: enough threads per item that each folds at most 8 of the
+  // max_chunks + 1 partial states; items split over workgroups of 512
+  {
+    int ph = 1;
+    while (ph < 8 && (pl.max_chunks + 1 + ph - 1) / ph > 8) ph *= 2;
+    const int items = bt->num_q_heads * (bt->head_dim / 8);
+    const int per = 512 / ph;
+    p.merge_phases = ph;
+    p.merge_parts = (items + per - 1) / per;
+  }
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);

@@ -70,6 +70,8 @@ struct StepParams {
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
   int shared, fused, nrg, chunk, max_chunks, n_groups, ctx_blocks;
+  int merge_phases;        // threads per merged item (slots split among them), power of 2
+  int merge_parts;         // merge workgroups per question
   float c;                 // scale * log2(e)
   float scale;
   double inv_freq[kMaxHalfDim];
