@@ -1,26 +1,30 @@
 // IPPD decode-step attention on gfx950: two launches per call.
 //
-//   attend_kernel       context units: shared-context attention, one
-//                       unnormalised partial softmax state (running max,
-//                       sum, weighted values) per query row and chunk;
-//   segment_merge_kernel  one workgroup per (question, kv head): in the fused
-//                       step it rotates and appends the token fed this step,
-//                       attends over the question's own segment, and merges
-//                       that state exactly with the context chunks' (splitting
-//                       only regroups the sums of attn_IPPD, Sec. 4.2).
+//   attend_kernel  context units (group, chunk, row group): shared-context
+//                  attention of 16*NW query rows over one chunk of context
+//                  tokens, one unnormalised partial softmax state (running
+//                  max, sum, weighted values) per row; then segment units,
+//                  seg_tpu tasks (question i, kv head g) each: in the fused
+//                  step rotate and append the token fed this step, and
+//                  attend the G query heads of group g over the question's
+//                  own segment (M_qtn, Sec. 4.1), the segment's tiles split
+//                  over the task's waves, whose states are combined in LDS;
+//   merge_kernel   combines each question's partial states exactly
+//                  (splitting only regroups the sums of attn_IPPD, Sec. 4.2)
+//                  and, in the fused step, advances its segment length.
 // The launch boundary orders the two, so no unit ever waits for another.
 //
 // A *group* is (prompt b, kv head g) for IPPD or (question i, kv head g) for
-// the standard baseline.  Context unit (group, chunk, row group): context
-// tokens [chunk*C, (chunk+1)*C) of prompt b against 16*NW query rows, the
+// the standard baseline.  A context unit streams context tokens
+// [chunk*C, (chunk+1)*C) of its group against 16*NW query rows, the
 // (question, head of group g) pairs of the prompt in order.  IPPD serves all
 // questions of the prompt from one pass over the chunk, so K_c and V_c come
 // from HBM once for all M_j queries (Sec. 4.3); the baseline serves the G
 // rows of one question and reads the context once per question (App. A.2.2,
 // PC+PA decode).  The workgroup streams 32-token tiles through an LDS ring
 // with LDS-DMA (global_load_lds_dwordx4: HBM -> LDS without passing through
-// registers), three tiles ahead of the compute; wave w owns rows 16w..16w+15
-// and reads its MFMA operands from the ring:
+// registers), several tiles ahead of the compute; wave w owns rows
+// 16w..16w+15 and reads its MFMA operands from the ring:
 //   S^T (keys x rows) = K Q^T       v_mfma_f32_16x16x32_bf16, A = 16 keys x 32 dims
 //   P^T = exp2(c * (S^T - m))       online softmax; the row max is reduced over
 //                                   the four 16-lane rows with permlane swaps
@@ -31,11 +35,8 @@
 // are XOR-swizzled in 16-byte chunks so that the 16 lanes of every ds_read
 // hit distinct bank groups of the 64-bank LDS.
 //
-// Segment (M_qtn, Sec. 4.1): four waves split the tiles of the question's
-// cached slots; its last key (the step's token, at virtual position
-// ctx_len[b] + seg_len[i]) is folded in from LDS, so the fused step never
-// waits for its own append.
 #include <float.h>
+#include <stddef.h>
 
 #include "ippd_device.h"
 #include "ippd_internal.h"
@@ -43,6 +44,8 @@
 namespace ippd {
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr float kRescaleLog2 = 8.f;   // lazy-rescale threshold of the online softmax
 
 // ---------------------------------------------------------------------------
 // MFMA operand traits: 8 contraction elements per lane per 32-wide step.
@@ -157,6 +160,19 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Wait until at most k * DPT vector memory operations are outstanding, for
+// a wave-uniform k in [0, K] (counts above 63 wait for 63: longer, never
+// shorter, than needed).
+template <int DPT, int K>
+__device__ __forceinline__ void wait_tiles(int k) {
+  if constexpr (K == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (k >= K) wait_vmcnt<(K * DPT < 63 ? K * DPT : 63)>();
+    else wait_tiles<DPT, K - 1>(k);
+  }
+}
+
 // Issue the DMA blocks of one tile (tokens [t0, t0+32) of [.., k1)) owned by
 // this wave: blocks wave, wave + NW, ...  Tokens past k1 are clamped to the
 // last valid one; the compute masks them.
@@ -208,15 +224,18 @@ __device__ __forceinline__ void row_init(RowState<D>& st) {
 
 // Fold one tile's scores (lane (lg, lr): tokens 8*lg + 4*kb + v of row lr)
 // into the state; returns P^T as the B operand of the PV product.  The
-// rescale by exp2(c*(m_old - m_new)) is skipped when no row's max moved,
-// where it would multiply by exactly 1.
+// running max m used as the exponent offset is raised only when some row's
+// tile max exceeds it by more than kRescaleLog2 (in log2 units): below that
+// the weights exp2(c*(s - m)) stay under 2^kRescaleLog2, harmless in fp32,
+// and the rescale of the sum and the values is skipped.  Any offset at or
+// below the true max gives the same normalised result.
 template <typename T, int D>
 __device__ __forceinline__ typename Mfma<T>::Frag softmax_step(const f32x4_t (&sc)[2], RowState<D>& st, float c) {
   float mx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
                    fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
   mx = xor16_max(mx);
   mx = xor32_max(mx);
-  if (__any(mx > st.m)) {
+  if (__any((mx - st.m) * c > kRescaleLog2)) {
     const float mn = fmaxf(st.m, mx);
     const float alpha = fast_exp2((st.m - (mn == -INFINITY ? 0.f : mn)) * c);
     st.l *= alpha;
@@ -301,266 +320,194 @@ __device__ __forceinline__ int usable_seg_len(const StepParams& p, int s) {
   return (s >= 1 && s <= p.seg_cap) ? s : -1;
 }
 
-// Query fragments (B operand) of one row (question qi, head h), in two
-// steps so that all loads can be issued, and waited for, before the tile DMA
-// starts: fetch_q loads q_new (fused step; plus the rotation frequencies of
-// the lane's pairs) or the given rotated queries; rotate_q rotates q_new at
-// pos.  Lane (lg, lr) holds dims 32*ds + 8*lg + u; pair j (j < D/2) is
-// (x_j, x_{j+D/2}), i.e. fragment ds and ds + DS/2.
-template <typename T, int D, bool FUSED>
-struct QFetch {
-  typename Mfma<T>::Frag f[D / 32];
-  double th[FUSED ? D / 8 : 1];
+// Prompt owning question i (q_start non-decreasing): the number of prompts
+// whose questions all precede i, with that prompt's layout fields and
+// whether they pass prompt_layout_ok and hold i.  Whole wave: up to 64
+// prompts come in one round of loads (lane l reads prompt l, and the owner's
+// fields are taken from its lane).
+struct PromptInfo {
+  int b, q0, q1, len;
+  int64_t off;
+  bool ok;
 };
 
-template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void fetch_q(QFetch<T, D, FUSED>& q, const StepParams& p, int qi, int h, int lg) {
-  using M = Mfma<T>;
-  constexpr int DS = D / 32;
-  const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8;
-#pragma unroll
-  for (int ds = 0; ds < DS; ++ds) q.f[ds] = M::load(src + 32 * ds);
-  if (FUSED) {
-#pragma unroll
-    for (int ds = 0; ds < DS / 2; ++ds)
-#pragma unroll
-      for (int u = 0; u < 8; ++u) q.th[8 * ds + u] = p.inv_freq[lg * 8 + 32 * ds + u];
+__device__ __forceinline__ PromptInfo find_prompt(const StepParams& p, int i, int lane) {
+  PromptInfo r;
+  if (p.B <= 64) {
+    const int bl = lane < p.B ? lane : p.B - 1;
+    const int q0 = p.q_start[bl], q1 = p.q_start[bl + 1], len = p.ctx_len[bl];
+    const int64_t off = p.ctx_off[bl];
+    r.b = __popcll(__ballot(lane < p.B && q1 <= i));
+    const int bs = r.b < p.B ? r.b : p.B - 1;
+    r.q0 = __builtin_amdgcn_readlane(q0, bs);
+    r.q1 = __builtin_amdgcn_readlane(q1, bs);
+    r.len = __builtin_amdgcn_readlane(len, bs);
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(off), bs);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(static_cast<uint64_t>(off) >> 32), bs);
+    r.off = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+  } else {
+    int n = 0;
+    for (int b0 = 0; b0 < p.B; b0 += 64) {
+      const int bb = b0 + lane;
+      n += __popcll(__ballot(bb < p.B && p.q_start[bb + 1] <= i));
+    }
+    r.b = n;
+    const int bs = n < p.B ? n : p.B - 1;
+    r.q0 = p.q_start[bs];
+    r.q1 = p.q_start[bs + 1];
+    r.len = p.ctx_len[bs];
+    r.off = p.ctx_off[bs];
   }
+  r.ok = r.b < p.B && r.q0 >= 0 && r.q1 >= r.q0 && r.q1 <= p.Nt && r.q1 - r.q0 <= p.max_questions &&
+         r.off >= 0 && (r.off & 7) == 0 && r.len >= 0 && r.len <= p.max_ctx_len && r.off + r.len <= p.pool &&
+         r.q0 <= i && i < r.q1;
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Row loads of a context unit: the lane's active flag, segment length and
+// query fragments.  They are issued with inline asm, ahead of the tile DMA,
+// so that the compiler's wait counting (which cannot see the DMA) does not
+// make their first use wait for the DMA too; wait_row_loads waits for exactly
+// them, its asm taking the destination registers as operands so that nothing
+// reads them earlier.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t gload_u8(const void* p) {
+  uint32_t r;
+  asm volatile("global_load_ubyte %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ uint32_t gload_b32(const void* p) {
+  uint32_t r;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ u32x4_t gload_b128(const void* p) {
+  u32x4_t r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
 }
 
 template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void rotate_q(typename Mfma<T>::Frag (&qf)[D / 32], const QFetch<T, D, FUSED>& q,
-                                         int64_t pos) {
+struct RowLoads {
+  static constexpr int QN = D * static_cast<int>(sizeof(T)) / 64;   // 16-byte query pieces per lane
+  static constexpr int QPF = static_cast<int>(sizeof(T)) / 2;       // pieces per 8-element fragment
+  static constexpr int TN = FUSED ? D / 16 : 0;                    // 16-byte pieces of the lane's D/8 frequencies
+  uint32_t a, s;
+  u32x4_t q[QN];
+  u32x4_t th[TN > 0 ? TN : 1];
+};
+
+// Lane (lg, lr) of row (question qi, head h): dims 32*ds + 8*lg + u of the
+// query (raw q_new in the fused step, rotated q_rot_in otherwise).
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void issue_row_loads(RowLoads<T, D, FUSED>& r, const StepParams& p, int qi, int h, int lg) {
+  using RL = RowLoads<T, D, FUSED>;
+  r.a = gload_u8(p.active + qi);
+  r.s = gload_b32(p.seg_len + qi);
+  const char* src = static_cast<const char*>(FUSED ? p.q_new : p.q_rot_in) +
+                    ((static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8) * static_cast<int64_t>(sizeof(T));
+#pragma unroll
+  for (int k = 0; k < RL::QN; ++k)
+    r.q[k] = gload_b128(src + (k / RL::QPF) * 32 * static_cast<int>(sizeof(T)) + (k % RL::QPF) * 16);
+  if constexpr (FUSED) {
+    // theta of pairs 32*ds + 8*lg + u, u = 0..7: 64 contiguous bytes per ds,
+    // read where the launch placed StepParams (the kernel's only argument)
+    const char* th = (const char*)__builtin_amdgcn_kernarg_segment_ptr() +   // address-space conversion
+                     offsetof(StepParams, inv_freq) + 8 * lg * sizeof(double);
+#pragma unroll
+    for (int k = 0; k < RL::TN; ++k) r.th[k] = gload_b128(th + (k / 4) * 32 * 8 + (k % 4) * 16);
+  }
+}
+
+template <int N, typename T, int D, bool FUSED>
+__device__ __forceinline__ void wait_row_loads(RowLoads<T, D, FUSED>& r) {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  using RL = RowLoads<T, D, FUSED>;
+  static_assert(RL::QN == 2 || RL::QN == 4 || RL::QN == 8, "query pieces");
+  static_assert(RL::TN == 0 || RL::TN == 4 || RL::TN == 8, "frequency pieces");
+  if constexpr (RL::QN == 2) {
+    asm volatile("s_waitcnt vmcnt(%4)" : "+v"(r.a), "+v"(r.s), "+v"(r.q[0]), "+v"(r.q[1]) : "n"(N));
+  } else {
+    asm volatile("s_waitcnt vmcnt(%6)"
+                 : "+v"(r.a), "+v"(r.s), "+v"(r.q[0]), "+v"(r.q[1]), "+v"(r.q[2]), "+v"(r.q[3])
+                 : "n"(N));
+    if constexpr (RL::QN == 8) asm volatile("" : "+v"(r.q[4]), "+v"(r.q[5]), "+v"(r.q[6]), "+v"(r.q[7]));
+  }
+  if constexpr (RL::TN >= 4) asm volatile("" : "+v"(r.th[0]), "+v"(r.th[1]), "+v"(r.th[2]), "+v"(r.th[3]));
+  if constexpr (RL::TN == 8) asm volatile("" : "+v"(r.th[4]), "+v"(r.th[5]), "+v"(r.th[6]), "+v"(r.th[7]));
+}
+
+// Query fragments (B operand) from the row loads, rotated at pos in the
+// fused step.  Pair j < D/2 is (x_j, x_{j+D/2}): fragments ds and ds + DS/2.
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], const RowLoads<T, D, FUSED>& r,
+                                          int64_t pos) {
   using M = Mfma<T>;
   constexpr int DS = D / 32;
-  if (!FUSED) {
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = q.f[ds];
-    return;
+  for (int ds = 0; ds < DS; ++ds) {
+    if constexpr (sizeof(T) == 2) {
+      qf[ds] = __builtin_bit_cast(typename M::Frag, r.q[ds]);
+    } else {
+      const f32x4_t x = __builtin_bit_cast(f32x4_t, r.q[2 * ds]), y = __builtin_bit_cast(f32x4_t, r.q[2 * ds + 1]);
+      qf[ds] = typename M::Frag{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+    }
   }
-  f32x8_t x[DS];
+  if constexpr (FUSED) {
 #pragma unroll
-  for (int ds = 0; ds < DS; ++ds) x[ds] = M::to_f32v(q.f[ds]);
-#pragma unroll
-  for (int ds = 0; ds < DS / 2; ++ds)
+  for (int ds = 0; ds < DS / 2; ++ds) {
+    f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       float cs, sn, xr, yr;
-      rope_cos_sin(pos, q.th[FUSED ? 8 * ds + u : 0], cs, sn);
-      rope_rotate(x[ds][u], x[ds + DS / 2][u], cs, sn, xr, yr);
-      x[ds][u] = xr;
-      x[ds + DS / 2][u] = yr;
+      const u32x4_t tp = r.th[4 * ds + u / 2];
+      const double theta = __hiloint2double(static_cast<int>(tp[2 * (u & 1) + 1]), static_cast<int>(tp[2 * (u & 1)]));
+      rope_cos_sin(pos, theta, cs, sn);
+      rope_rotate(x[u], y[u], cs, sn, xr, yr);
+      x[u] = xr;
+      y[u] = yr;
     }
-#pragma unroll
-  for (int ds = 0; ds < DS; ++ds) qf[ds] = M::from_f32(x[ds]);
+    qf[ds] = M::from_f32(x);
+    qf[ds + DS / 2] = M::from_f32(y);
+  }
+  }
 }
 
 // ---------------------------------------------------------------------------
-// Segment task (question i of prompt b, kv head g; one wave), run by the
-// context units once their chunk is done.  Fused step: rotate the step's
-// key at virtual position ctx_len + seg_len[i] and append it with its value;
-// the task's own attention folds that key in from LDS after streaming the
-// cached slots, so it never waits for the store.  Attention-only calls fold
-// slot seg_len[i] - 1 the same way, so both give identical sums.
-// ---------------------------------------------------------------------------
-template <typename T, int D>
-struct SegScratch {
-  static constexpr int QROW = D * sizeof(T) + 16;   // padded: the 16 lanes of a read hit distinct banks
-  alignas(16) unsigned char q[16 * QROW];           // rotated queries of the G heads (rows >= G zero)
-  alignas(16) T k[D];                               // the last key and value
-  alignas(16) T v[D];
-};
-
-template <typename T, int D, bool FUSED>
-__device__ void segment_task(const StepParams& p, SegScratch<T, D>& ws, int i, int ctx_len, int g, int lane) {
-  using M = Mfma<T>;
-  using Frag = typename M::Frag;
-  using SS = SegScratch<T, D>;
-  constexpr int DS = D / 32, DB = D / 16;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int G = p.G;
-  const int sraw = p.seg_len[i];
-  const int s = usable_seg_len(p, sraw);
-  if (s < 0) {
-    if (lane == 0 && g == 0) raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
-    return;
-  }
-  const int64_t sg = static_cast<int64_t>(i) * p.Hkv + g;
-  T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
-  T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
-  const int64_t pos = static_cast<int64_t>(ctx_len) + s;
-  {
-    // query rows: lane (lg, lr) holds head g*G + lr, dims 32*ds + 8*lg + u
-    const int h = g * G + (lr < G ? lr : 0);
-    const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + h) * D + lg * 8;
-    Frag qf[DS];
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
-    if (FUSED) {
-      // rotate pairs (j, j + D/2), j = 32*ds + 8*lg + u, at pos
-#pragma unroll
-      for (int ds = 0; ds < DS / 2; ++ds) {
-        f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          float cs, sn, xr, yr;
-          rope_cos_sin(pos, p.inv_freq[lg * 8 + 32 * ds + u], cs, sn);
-          rope_rotate(x[u], y[u], cs, sn, xr, yr);
-          x[u] = xr;
-          y[u] = yr;
-        }
-        qf[ds] = M::from_f32(x);
-        qf[ds + DS / 2] = M::from_f32(y);
-      }
-    }
-    if (lr >= G) {
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) qf[ds] = M::zero();
-    } else if (FUSED && p.q_rot_out != nullptr) {
-      T* qo = static_cast<T*>(p.q_rot_out) + (static_cast<int64_t>(i) * p.Hq + h) * D + lg * 8;
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) store8<T>(qo + 32 * ds, qf[ds]);
-    }
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) store8<T>(reinterpret_cast<T*>(ws.q + lr * SS::QROW) + 32 * ds + lg * 8, qf[ds]);
-  }
-  if (FUSED) {
-    const T* kn = static_cast<const T*>(p.k_new) + sg * D;
-    const T* vn = static_cast<const T*>(p.v_new) + sg * D;
-    for (int jj = lane; jj < D / 2; jj += 64) {
-      float cs, sn, x, y;
-      rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
-      rope_rotate(to_f32<T>(kn[jj]), to_f32<T>(kn[jj + D / 2]), cs, sn, x, y);
-      const T xk = from_f32<T>(x), yk = from_f32<T>(y);
-      skp[static_cast<int64_t>(s) * D + jj] = xk;
-      skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
-      ws.k[jj] = xk;
-      ws.k[jj + D / 2] = yk;
-    }
-    for (int d = lane; d < D; d += 64) {
-      const T v = vn[d];
-      svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
-      ws.v[d] = v;
-    }
-  } else {
-    for (int d = lane; d < D; d += 64) {
-      ws.k[d] = skp[static_cast<int64_t>(s - 1) * D + d];
-      ws.v[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
-    }
-  }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-
-  RowState<D> st;
-  row_init(st);
-  const float c = p.c;
-  const unsigned char* qrow = ws.q + lr * SS::QROW + lg * 8 * sizeof(T);
-  const int mem = FUSED ? s : s - 1;            // cached slots before the last key
-  const int ntiles = (mem + 31) >> 5;
-  const int mlast = max(mem - 1, 0);
-  // the segment bases are wave-uniform: loads take them as scalar bases plus
-  // 32-bit lane offsets (a segment holds < 2^31 elements)
-  const T* __restrict__ kseg = skp;
-  const T* __restrict__ vseg = svp;
-  for (int t = 0; t < ntiles; ++t) {
-    const int t0 = 32 * t;
-    Frag kf[2][DS], vf[DB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const uint32_t ko = static_cast<uint32_t>(min(t0 + tile_token(kb, lr), mlast) * D + lg * 8);
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = M::load(kseg + (ko + 32 * ds));
-    }
-    const uint32_t vo = static_cast<uint32_t>(min((t0 >> 3) + lg, mlast >> 3) * 8 * D + lr * 8);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) vf[db] = M::load(vseg + (vo + 16 * db * 8));
-    const int n = min(mem - t0, 32);
-    f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const Frag qf = M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T)));
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) sc[kb] = M::mma(kf[kb][ds], qf, sc[kb]);
-    }
-    if (n < 32) mask_scores(sc, n, lg);
-    const Frag pf = softmax_step<T, D>(sc, st, c);
-    const int keep = min(max(n - 8 * lg, 0), 8);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
-      st.o[db] = M::mma(v, pf, st.o[db]);
-    }
-  }
-  {
-    // the last key: score = q_row . k, folded in as one more token
-    float dot = 0.f;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * sizeof(T))));
-      const f32x8_t kv = M::to_f32v(M::load(ws.k + 32 * ds + lg * 8));
-#pragma unroll
-      for (int u = 0; u < 8; ++u) dot = fmaf(qv[u], kv[u], dot);
-    }
-    dot = xor16_sum(dot);
-    dot = xor32_sum(dot);
-    if (__any(dot > st.m)) {
-      const float mn = fmaxf(st.m, dot);
-      const float alpha = fast_exp2((st.m - mn) * c);
-      st.l *= alpha;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) st.o[db] *= alpha;
-      st.m = mn;
-    }
-    const float pn = fast_exp2((dot - st.m) * c);
-    if (lg == 0) st.l += pn;                 // one lane per row: the sum is reduced over lg below
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) st.o[db][v] = fmaf(pn, to_f32<T>(ws.v[16 * db + 4 * lg + v]), st.o[db][v]);
-  }
-  float l = xor16_sum(st.l);
-  st.l = xor32_sum(l);
-  if (lr < G) publish_rows<D>(p, st, (static_cast<int64_t>(p.max_chunks) * p.Nt + i) * p.Hq + g * G + lr, lg);
-}
-
-// ---------------------------------------------------------------------------
-// attend_kernel.  The first ctx_blocks workgroups are context units:
-// blockIdx -> slice (XCD) = blockIdx & 7, local = blockIdx >> 3;
-// consecutive locals of a slice are the row groups of one chunk (they share
-// its tiles through that XCD's L2) and chunks are dealt to the slices round
-// robin.  The remaining workgroups are segment units, NW segment tasks each
-// (task (b, j, g): question slot j of prompt b, kv head g).  Workgroups are
-// dispatched in order, so segment units start as context units retire and
-// fill the tail of the context work.
+// LDS of one workgroup.  Context units use main as the tile ring.  Segment
+// units hold, per task, the query rows and the rotation table in it, then
+// the waves' states to be combined.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int NW, int NS>
-union AttendShared {
-  alignas(16) unsigned char ring[NS * 2 * 32 * D * sizeof(T)];
-  SegScratch<T, D> seg[NW];
+struct UnitLds {
+  static constexpr int RING = NS * Ring<T, D, NS>::STAGE;
+  static constexpr int QROW = D * static_cast<int>(sizeof(T)) + 16;   // padded: a read's 16 lanes hit distinct banks
+  static constexpr int QAREA = 16 * QROW;                              // one task's query rows
+  static constexpr int TASK = QAREA + (D / 2) * 8;                     // + (cos, sin) of its position
+  static constexpr int MAIN = RING;
+  static_assert(NW * TASK <= MAIN, "segment tasks must fit");
+  alignas(16) unsigned char main[MAIN];
+  alignas(16) T k[NW][D];      // per task: the segment's last key (the step's token) and value
+  alignas(16) T v[NW][D];
+  float2 ml[NW][16];           // per wave: (max, sum) of its segment rows
+  float slast[NW][16];         // per task: score of the last key per row
+  int live[NW];                // per task: served this call
 };
 
+// ---------------------------------------------------------------------------
+// Context unit.  blockIdx -> slice (XCD) = blockIdx & 7, local = blockIdx >> 3;
+// consecutive locals of a slice are the row groups of one chunk (they share
+// its tiles through that XCD's L2) and chunks are dealt to the slices round
+// robin.
+// ---------------------------------------------------------------------------
 template <typename T, int D, int NW, int NS, bool FUSED>
-__global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
+__device__ __forceinline__ void context_unit(const StepParams& p, unsigned char* ring, int wave, int lane) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
   constexpr int RW = 16 * NW, DPT = RG::BLOCKS / NW;
-  __shared__ AttendShared<T, D, NW, NS> sh;
-  unsigned char* ring = sh.ring;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int P0 = RG::NS - 1 < 3 ? RG::NS - 1 : 3;      // tiles issued before the queries are rotated
   const int lr = lane & 15, lg = lane >> 4;
-  if (static_cast<int>(blockIdx.x) >= p.ctx_blocks) {
-    // segment unit: task (b, j, g) per wave
-    const int task = (static_cast<int>(blockIdx.x) - p.ctx_blocks) * NW + wave;
-    const int g = task % p.Hkv, bj = task / p.Hkv;
-    const int b = bj / p.max_questions, j = bj - b * p.max_questions;
-    if (b >= p.B || !prompt_layout_ok(p, b)) return;
-    const int i = p.q_start[b] + j;
-    if (i >= p.q_start[b + 1] || !p.active[i]) return;
-    segment_task<T, D, FUSED>(p, sh.seg[wave], i, p.ctx_len[b], g, lane);
-    return;
-  }
   const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int cl = local / p.nrg, rg = local - cl * p.nrg;
   const int cglob = cl * 8 + slice;
@@ -574,90 +521,354 @@ __global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
   } else {
     g = grp / p.Nt;
     qa = grp - g * p.Nt;
-    b = prompt_of(p.q_start, p.B, qa);
+    b = find_prompt(p, qa, lane).b;
+    if (b >= p.B) {
+      if (threadIdx.x == 0 && chunk == 0) raise_flag(p.err_flag, kFlagBadLayout);
+      return;
+    }
   }
   if (!prompt_layout_ok(p, b)) {
     if (threadIdx.x == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
     return;
   }
-  if (p.shared) { qa = p.q_start[b]; qb = p.q_start[b + 1]; } else { qb = qa + 1; }
+  if (p.shared) {
+    qa = p.q_start[b];
+    qb = p.q_start[b + 1];
+  } else {
+    qb = qa + 1;
+  }
   const int G = p.G;
-  const int nq = qb - qa;
-  const int nrows = nq * G;
+  const int nrows = (qb - qa) * G;
   const int row0 = rg * RW;
   const int ctx_len = p.ctx_len[b];
   if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len || row0 >= nrows) return;
-  {
-    const int64_t off = p.ctx_off[b];
-    const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
-    const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
-    const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
-    const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
-    const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
-    const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-    // this lane's row: question qa + row / G, head g*G + row % G.  Its loads
-    // all go out, and land, before the tile DMA: queued behind the DMA of
-    // every workgroup they would wait for all of it.
-    const int row = row0 + 16 * wave + lr;
-    const bool in_range = row < nrows;
-    const int rr = in_range ? row : nrows - 1;
-    const int qi = qa + rr / G, h = g * G + rr % G;
-    const bool a_raw = p.active[qi] != 0;
-    const int s_raw = FUSED ? p.seg_len[qi] : 0;
-    QFetch<T, D, FUSED> qraw;
-    fetch_q<T, D, FUSED>(qraw, p, qi, h, lg);
-    wait_vmcnt<0>();
+  const int64_t off = p.ctx_off[b];
+  const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
+  const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
+  const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
+  const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
+  const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-    // the first NS-1 tiles; the rotation below overlaps with them
+  // this lane's row: question qa + row / G, head g*G + row % G
+  const int row = row0 + 16 * wave + lr;
+  const bool in_range = row < nrows;
+  const int rr = in_range ? row : nrows - 1;
+  const int qi = qa + rr / G, h = g * G + rr % G;
+  RowLoads<T, D, FUSED> rl;
+  issue_row_loads<T, D, FUSED>(rl, p, qi, h, lg);
+  // exactly P0 tiles go out before the one wait for the row loads (a unit
+  // with fewer tiles fetches its last tile again): a single wait with a
+  // fixed count leaves the compiler no reason to copy the loaded registers
+  // before it.  The extra DMAs are younger than every real tile, so the
+  // ring's waits below stay sufficient.
 #pragma unroll
-    for (int t = 0; t < RG::NS - 1; ++t)
-      issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
+  for (int t = 0; t < P0; ++t)
+    issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
+  wait_row_loads<(P0 * DPT < 63 ? P0 * DPT : 63)>(rl);
 
-    const bool act = in_range && a_raw;
-    const bool live = __any(act);                   // wave-uniform
-    typename M::Frag qf[D / 32];
-    rotate_q<T, D, FUSED>(qf, qraw, static_cast<int64_t>(ctx_len) + s_raw);
-    if (!act) {
+  const int s_raw = static_cast<int>(rl.s);
+  const bool act = in_range && rl.a != 0u && usable_seg_len(p, s_raw) >= 0;
+  const bool live = __any(act);                    // wave-uniform
+  typename M::Frag qf[D / 32];
+  row_query<T, D, FUSED>(qf, rl, static_cast<int64_t>(ctx_len) + s_raw);
+  if (!act) {
 #pragma unroll
-      for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
-    }
-    RowState<D> st;
-    row_init(st);
-    const float c = p.c;
-
-    // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
-    // is refilled with tile t + NS - 1
-    const int last = ntiles - 1;
-    const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
-    for (int t = 0; t < ntiles; ++t) {
-      // tile t's blocks are this thread's oldest DMAs (at most 63 can be
-      // tracked: beyond that the wait is merely longer than needed)
-      wait_vmcnt<((RG::NS - 2) * DPT < 63 ? (RG::NS - 2) * DPT : 63)>();
-      __syncthreads();
-      const int tn = t + RG::NS - 1;
-      issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * min(tn, last), k1,
-                               wave, lane);
-      if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
-    }
-    wait_vmcnt<0>();                                // no LDS-DMA may outlive the workgroup
-
-    float l = xor16_sum(st.l);
-    st.l = xor32_sum(l);
-    if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
+    for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
   }
+#pragma unroll
+  for (int t = P0; t < RG::NS - 1; ++t)
+    if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane);
+  RowState<D> st;
+  row_init(st);
+  const float c = p.c;
 
+  // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
+  // is refilled with tile t + NS - 1
+  const int last = ntiles - 1;
+  const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
+  for (int t = 0; t < ntiles; ++t) {
+    // tile t's blocks are this thread's oldest outstanding DMAs; those of
+    // tiles t+1 .. min(t+NS-2, last) are younger
+    wait_tiles<DPT, RG::NS - 2>(min(last - t, RG::NS - 2));
+    __syncthreads();
+    const int tn = t + RG::NS - 1;
+    if (tn <= last)
+      issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane);
+    if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+  }
+  wait_vmcnt<0>();                                  // no LDS-DMA may outlive the workgroup
+
+  float l = xor16_sum(st.l);
+  st.l = xor32_sum(l);
+  if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
 }
 
 // ---------------------------------------------------------------------------
-// merge_kernel: question i = q_start[b] + j is served by merge_parts
-// workgroups of kMergeThreads threads.  Item (head h, dims d0..d0+7) of the
-// question combines its context chunks and its segment state:
+// Segment unit (question i, kv head g).  The segment's cached slots are
+// streamed in 32-token tiles, wave w taking tiles w, w + sw, ...; its last
+// key (the step's token, at virtual position ctx_len[b] + seg_len[i], or
+// slot seg_len[i] - 1 in attention-only calls) is folded in from LDS, so the
+// fused step never waits for its own append.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__device__ __forceinline__ void load_seg_tile(typename Mfma<T>::Frag (&kf)[2][D / 32], typename Mfma<T>::Frag (&vf)[D / 16],
+                                              const T* __restrict__ kseg, const T* __restrict__ vseg, int t, int mlast,
+                                              int lr, int lg) {
+  using M = Mfma<T>;
+  const int t0 = 32 * t;
+  // the segment bases are wave-uniform: scalar base plus 32-bit lane offsets
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const uint32_t ko = static_cast<uint32_t>(min(t0 + tile_token(kb, lr), mlast) * D + lg * 8);
+#pragma unroll
+    for (int ds = 0; ds < D / 32; ++ds) kf[kb][ds] = M::load(kseg + (ko + 32 * ds));
+  }
+  const uint32_t vo = static_cast<uint32_t>(min((t0 >> 3) + lg, mlast >> 3) * 8 * D + lr * 8);
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) vf[db] = M::load(vseg + (vo + 16 * db * 8));
+}
+
+template <typename T, int D, int NW, int NS, bool FUSED>
+__device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, NW, NS>& sh, int u, int wave,
+                                             int lane) {
+  using M = Mfma<T>;
+  using Frag = typename M::Frag;
+  using L = UnitLds<T, D, NW, NS>;
+  constexpr int DS = D / 32, DB = D / 16, E = static_cast<int>(sizeof(T));
+  const int lr = lane & 15, lg = lane >> 4;
+  const int G = p.G;
+  // seg_tpu tasks (question i, kv head g) per unit, wpt waves each
+  const int tpu = p.seg_tpu, wpt = NW / tpu;
+  const int k = wave / wpt, ww = wave - k * wpt;
+  const int task = u * tpu + k;
+  const bool valid = task < p.Nt * p.Hkv;
+  const int tsk = valid ? task : 0;
+  const int i = tsk / p.Hkv, g = tsk - i * p.Hkv;
+  const int64_t sg = static_cast<int64_t>(i) * p.Hkv + g;
+  // the leader's loads need only (i, g): issued here, in a block that does
+  // not dominate their uses, they go out with the prompt and segment-length
+  // loads below and share their round trip
+  const int hq = g * G + (lr < G ? lr : 0);
+  Frag qf[DS];
+  T kraw[2], vraw[2];
+  if (ww == 0) {
+    const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + hq) * D + lg * 8;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
+    if (FUSED) {
+      const T* kn = static_cast<const T*>(p.k_new) + sg * D;
+      const T* vn = static_cast<const T*>(p.v_new) + sg * D;
+      const int jj = lane % (D / 2);
+      kraw[0] = kn[jj];
+      kraw[1] = kn[jj + D / 2];
+      vraw[0] = vn[lane % D];
+      vraw[1] = vn[(lane + 64) % D];
+    }
+  }
+  const PromptInfo pi = find_prompt(p, i, lane);
+  const int sraw = p.seg_len[i];
+  const bool act = valid && p.active[i] != 0;
+  const int s = usable_seg_len(p, sraw);
+  if (act && s < 0 && g == 0 && ww == 0 && lane == 0)
+    raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
+  const bool live = act && s >= 0 && pi.ok;        // bad layouts are flagged by the context units
+  T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
+  T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
+  const int mem = FUSED ? s : s - 1;               // cached slots before the last key
+  const int ntiles = live ? (mem + 31) >> 5 : 0;
+  const int mlast = max(mem - 1, 0);
+  // sw waves of the task hold states to combine (all tasks' states must fit
+  // main); tile t goes to wave (t + 1) % sw, so the leader, busy with the
+  // queries first, takes tiles last
+  const int sw = min(wpt, L::MAIN / (G * (D + 4) * 4) / tpu);
+  const int first = ww < sw ? (ww + sw - 1) % sw : ntiles;
+  unsigned char* qrows = sh.main + k * L::TASK;
+  const unsigned char* qrow = qrows + lr * L::QROW + lg * 8 * E;
+  Frag kf[2][DS], vf[DB];
+  if (ww == 0) {
+    if (lane == 0) sh.live[k] = live ? 1 : 0;
+    if (live) {
+      // query rows of the G heads (rows >= G zero), rotated at the step
+      // token's virtual position ctx_len[b] + seg_len[i] in the fused step
+      const int h = hq;
+      float2* rot = reinterpret_cast<float2*>(qrows + L::QAREA);
+      if (FUSED) {
+        const int64_t pos = static_cast<int64_t>(pi.len) + s;
+        for (int jj = lane; jj < D / 2; jj += 64) {
+          float cs, sn;
+          rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
+          rot[jj] = make_float2(cs, sn);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int ds = 0; ds < DS / 2; ++ds) {
+          f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
+#pragma unroll
+          for (int uu = 0; uu < 8; ++uu) {
+            const float2 cs = rot[32 * ds + 8 * lg + uu];
+            float xr, yr;
+            rope_rotate(x[uu], y[uu], cs.x, cs.y, xr, yr);
+            x[uu] = xr;
+            y[uu] = yr;
+          }
+          qf[ds] = M::from_f32(x);
+          qf[ds + DS / 2] = M::from_f32(y);
+        }
+      }
+      if (lr >= G) {
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) qf[ds] = M::zero();
+      } else if (FUSED && p.q_rot_out != nullptr) {
+        T* qo = static_cast<T*>(p.q_rot_out) + (static_cast<int64_t>(i) * p.Hq + h) * D + lg * 8;
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) store8<T>(qo + 32 * ds, qf[ds]);
+      }
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) store8<T>(reinterpret_cast<T*>(qrows + lr * L::QROW) + 32 * ds + lg * 8, qf[ds]);
+      if (FUSED) {
+        // rotate the step's key at pos; append it and its value at slot s
+        if (lane < D / 2) {
+          const int jj = lane;
+          const float2 cs = rot[jj];
+          float x, y;
+          rope_rotate(to_f32<T>(kraw[0]), to_f32<T>(kraw[1]), cs.x, cs.y, x, y);
+          const T xk = from_f32<T>(x), yk = from_f32<T>(y);
+          skp[static_cast<int64_t>(s) * D + jj] = xk;
+          skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
+          sh.k[k][jj] = xk;
+          sh.k[k][jj + D / 2] = yk;
+        }
+#pragma unroll
+        for (int r = 0; r < (D + 63) / 64; ++r) {
+          const int d = lane + 64 * r;
+          if (d < D) {
+            const T v = vraw[r];
+            svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
+            sh.v[k][d] = v;
+          }
+        }
+      } else {
+        for (int d = lane; d < D; d += 64) {
+          sh.k[k][d] = skp[static_cast<int64_t>(s - 1) * D + d];
+          sh.v[k][d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // score of the last key: q_row . k, reduced over the four lanes of a row
+      float dot = 0.f;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * E)));
+        const f32x8_t kv = M::to_f32v(M::load(&sh.k[k][32 * ds + lg * 8]));
+#pragma unroll
+        for (int uu = 0; uu < 8; ++uu) dot = fmaf(qv[uu], kv[uu], dot);
+      }
+      dot = xor16_sum(dot);
+      dot = xor32_sum(dot);
+      if (lg == 0 && lr < G) sh.slast[k][lr] = dot;
+    }
+  } else if (first < ntiles) {
+    load_seg_tile<T, D>(kf, vf, skp, svp, first, mlast, lr, lg);   // in flight across the barrier
+  }
+  __syncthreads();                                 // query rows, last keys and their scores are in LDS
+
+  RowState<D> st;
+  row_init(st);
+  const float c = p.c;
+  for (int t = first; t < ntiles; t += sw) {
+    asm volatile("" ::: "memory");                // query rows are re-read from LDS, not held in registers
+    if (ww == 0 || t != first) load_seg_tile<T, D>(kf, vf, skp, svp, t, mlast, lr, lg);
+    const int n = min(mem - 32 * t, 32);
+    f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const Frag q = M::load(reinterpret_cast<const T*>(qrow + 32 * ds * E));
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sc[kb] = M::mma(kf[kb][ds], q, sc[kb]);
+    }
+    if (n < 32) mask_scores(sc, n, lg);
+    const Frag pf = softmax_step<T, D>(sc, st, c);
+    const int keep = min(max(n - 8 * lg, 0), 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
+      st.o[db] = M::mma(v, pf, st.o[db]);
+    }
+  }
+  float l = xor16_sum(st.l);
+  st.l = xor32_sum(l);
+  __syncthreads();                                 // the query rows are dead
+  if (live && ww < sw && lr < G) {
+    float* o = reinterpret_cast<float*>(sh.main) + ((k * sw + ww) * G + lr) * (D + 4) + 4 * lg;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4_t*>(o + 16 * db) = st.o[db];
+    if (lg == 0) sh.ml[k * sw + ww][lr] = make_float2(st.m, st.l);
+  }
+  __syncthreads();
+  // combine each task's wave states and its last key: item (task, row r, dims d0..d0+7)
+  const int per_task = G * (D / 8);
+  for (int e = threadIdx.x; e < tpu * per_task; e += 64 * NW) {
+    const int kk = e / per_task, er = e - kk * per_task;
+    if (!sh.live[kk]) continue;
+    const int r = er / (D / 8), d0 = (er - r * (D / 8)) * 8;
+    const float sl = sh.slast[kk][r];
+    float m = sl;
+    for (int w = 0; w < sw; ++w) m = fmaxf(m, sh.ml[kk * sw + w][r].x);
+    const float fl = fast_exp2((sl - m) * c);
+    float lsum = fl;
+    f32x4_t a0, a1;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      a0[v] = fl * to_f32<T>(sh.v[kk][d0 + v]);
+      a1[v] = fl * to_f32<T>(sh.v[kk][d0 + 4 + v]);
+    }
+    for (int w = 0; w < sw; ++w) {
+      const float2 mlw = sh.ml[kk * sw + w][r];
+      const float f = fast_exp2((mlw.x - m) * c);  // 0 for a wave without tiles (max -inf)
+      lsum = fmaf(f, mlw.y, lsum);
+      const float* o = reinterpret_cast<const float*>(sh.main) + ((kk * sw + w) * G + r) * (D + 4) + d0;
+      a0 += f * *reinterpret_cast<const f32x4_t*>(o);
+      a1 += f * *reinterpret_cast<const f32x4_t*>(o + 4);
+    }
+    const int tk = u * tpu + kk;
+    const int ik = tk / p.Hkv, gk = tk - ik * p.Hkv;
+    const int64_t slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + ik) * p.Hq + gk * G + r;
+    f32x4_t* dst = reinterpret_cast<f32x4_t*>(p.part_acc + slot * D + d0);
+    dst[0] = a0;
+    dst[1] = a1;
+    if (d0 == 0) *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(m, lsum);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// attend_kernel: context units (blockIdx < ctx_blocks), then segment units.
+// Workgroups are dispatched in order, so segment units start as context
+// units retire and fill the tail of the context work.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int NW, int NS, bool FUSED>
+__global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
+  __shared__ UnitLds<T, D, NW, NS> sh;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int blk = static_cast<int>(blockIdx.x);
+  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED>(p, sh.main, wave, lane);
+  else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks, wave, lane);
+}
+
+// ---------------------------------------------------------------------------
+// merge_kernel: question i is served by merge_parts workgroups of
+// kMergeThreads threads.  Item (head h, dims d0..d0+7) of the question
+// combines its context chunks and its segment state:
 //   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l.
 // With P = merge_phases, a workgroup takes kMergeThreads / P items and P
 // threads per item, thread phase f folding slots f, f + P, ...; the P states
-// of an item are then combined through LDS.  The partial states are requested
-// together with the question's active flag and segment length.
+// of an item are then combined through LDS.
 // ---------------------------------------------------------------------------
 constexpr int kMergeThreads = 512;
 constexpr int kMergeBatch = 8;       // partial states in flight per thread
@@ -687,19 +898,17 @@ struct MergeAcc {
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
   __shared__ __attribute__((aligned(16))) float mp[kMergeThreads * 12];   // (m, l, -, -, 8 values) per thread
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int P = p.merge_phases, per = kMergeThreads / P;
-  const int part = blockIdx.x % p.merge_parts, bj = blockIdx.x / p.merge_parts;
-  const int b = bj / p.max_questions, j = bj - b * p.max_questions;
-  if (!prompt_layout_ok(p, b)) return;             // flagged by the context units
-  const int i = p.q_start[b] + j;
-  if (i >= p.q_start[b + 1]) return;
-  const int nc = min((p.ctx_len[b] + p.chunk - 1) / p.chunk, p.max_chunks);
+  const int i = blockIdx.x / p.merge_parts, part = blockIdx.x - i * p.merge_parts;
+  const PromptInfo pi = find_prompt(p, i, lane);
+  const bool act = p.active[i] != 0;
+  const int s = usable_seg_len(p, p.seg_len[i]);
+  if (!act || s < 0 || !pi.ok) return;             // workgroup-uniform; flagged elsewhere
+  const int nc = min((pi.len + p.chunk - 1) / p.chunk, p.max_chunks);
   const int nslot = nc + 1;                        // chunks, then the segment
   const float c = p.c;
   const int items = p.Hq * (D / 8);
-  const bool act = p.active[i] != 0;
-  const int s = usable_seg_len(p, p.seg_len[i]);
   const int f = tid / per, local = tid - f * per;
   const int e = part * per + local;                // this thread's item
   const bool has = e < items;
@@ -710,21 +919,19 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
     float2 ml[kMergeBatch];
     f32x4_t x0[kMergeBatch], x1[kMergeBatch];
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) {
-      const int k = min(k0 + P * u, nslot - 1);
+    for (int uu = 0; uu < kMergeBatch; ++uu) {
+      const int k = min(k0 + P * uu, nslot - 1);
       const int ck = k < nc ? k : p.max_chunks;
       const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
-      ml[u] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
+      ml[uu] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
       const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
-      x0[u] = src[0];
-      x1[u] = src[1];
+      x0[uu] = src[0];
+      x1[uu] = src[1];
     }
-    if (!act || s < 0) break;                      // inactive or skipped: nothing to write
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u)
-      if (k0 + P * u < nslot) acc.fold(ml[u].x, ml[u].y, x0[u], x1[u], c);
+    for (int uu = 0; uu < kMergeBatch; ++uu)
+      if (k0 + P * uu < nslot) acc.fold(ml[uu].x, ml[uu].y, x0[uu], x1[uu], c);
   }
-  if (!act || s < 0) return;                       // workgroup-uniform
   if (P > 1) {
     float* dst = mp + tid * 12;
     dst[0] = acc.m;
@@ -768,8 +975,8 @@ static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
 }
 
 // Ring depth: 4 stages (two workgroups per CU) in general; 8 (one per CU,
-// every tile of a short unit in flight at once) when the grid fits the chip
-// in one wave.  fp32 at D = 128 has 32 KB stages: 2 or 4.
+// every tile of a short unit in flight at once) when the context units fit
+// the chip in one wave.  fp32 at D = 128 has 32 KB stages: 2 or 4.
 template <typename T, int D, int NW>
 static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStream_t s) {
   constexpr int base = (2 * 32 * D * sizeof(T)) > 16384 ? 2 : 4;
@@ -777,24 +984,28 @@ static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStre
 }
 
 template <typename T, int D>
-static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
-  hipError_t e = hipSuccess;
-  if (grid > 0) {
-    switch (waves) {
-      case 1: e = launch_depth<T, D, 1>(deep, grid, p, s); break;
-      case 2: e = launch_depth<T, D, 2>(deep, grid, p, s); break;
-      case 4: e = launch_depth<T, D, 4>(deep, grid, p, s); break;
-      default: e = launch_depth<T, D, 8>(deep, grid, p, s); break;
-    }
-    if (e != hipSuccess) return e;
+static hipError_t launch_waves(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  switch (waves) {
+    case 1: return launch_depth<T, D, 1>(deep, grid, p, s);
+    case 2: return launch_depth<T, D, 2>(deep, grid, p, s);
+    case 4: return launch_depth<T, D, 4>(deep, grid, p, s);
+    default:
+      // the planner gives fp32 at D = 128 at most four waves
+      if constexpr (sizeof(T) == 4 && D == 128) return hipErrorInvalidValue;
+      else return launch_depth<T, D, 8>(deep, grid, p, s);
   }
-  const unsigned nblk = static_cast<unsigned>(p.B) * p.max_questions * p.merge_parts;
-  merge_kernel<D><<<nblk, kMergeThreads, 0, s>>>(p);
+}
+
+template <typename T, int D>
+static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  hipError_t e = launch_waves<T, D>(waves, deep, grid, p, s);
+  if (e != hipSuccess) return e;
+  merge_kernel<D><<<static_cast<unsigned>(p.Nt) * p.merge_parts, kMergeThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
 hipError_t launch_step(int dtype, int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
-  if (p.Nt == 0) return hipSuccess;
+  if (p.Nt == 0 || grid == 0) return hipSuccess;
   if (dtype == 0)
     return p.D == 64 ? launch_d<float, 64>(waves, deep, grid, p, s) : launch_d<float, 128>(waves, deep, grid, p, s);
   return p.D == 64 ? launch_d<uint16_t, 64>(waves, deep, grid, p, s)

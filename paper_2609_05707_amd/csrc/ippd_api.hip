@@ -77,6 +77,8 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   // waves per workgroup; a context unit covers 16 rows per wave
   int waves = bt->tile_rows / 16;
   if (waves == 0) waves = max_rows <= 16 ? 1 : (max_rows <= 32 ? 2 : (max_rows <= 64 ? 4 : 8));
+  // fp32 at D = 128: the operands of eight waves do not fit their registers
+  if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && waves > 4) waves = 4;
   const int nrg = static_cast<int>((max_rows + 16 * waves - 1) / (16 * waves));
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
@@ -90,11 +92,16 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   }
   const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
   const int64_t ctx_blocks = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
-  const int64_t seg_tasks = static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads;
-  const int64_t grid = ctx_blocks + (seg_tasks + waves - 1) / waves;
-  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) ||
-      static_cast<int64_t>(bt->num_prompts) * bt->max_questions * bt->num_kv_heads * 8 > (1ll << 31) - 1)
-    return false;
+  // segment tasks (question, kv head): about two units per compute unit, at
+  // most `waves` tasks per unit, and all tasks' wave states must fit the
+  // smallest LDS ring (32 KB)
+  const int64_t seg_tasks = static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
+  const int64_t state_bytes = static_cast<int64_t>(G) * (bt->head_dim + 4) * 4;
+  int tpu = 1;
+  while (tpu < waves && seg_tasks / (2 * tpu) >= 2 * compute_units() && 2 * tpu * state_bytes <= 32768) tpu *= 2;
+  const int64_t seg_blocks = (seg_tasks + tpu - 1) / tpu;
+  const int64_t grid = ctx_blocks + seg_blocks;
+  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
   pl->nrg = nrg;
@@ -103,6 +110,8 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->n_groups = static_cast<int>(n_groups);
   pl->grid = static_cast<int>(grid);
   pl->ctx_blocks = static_cast<int>(ctx_blocks);
+  pl->seg_blocks = static_cast<int>(seg_blocks);
+  pl->seg_tpu = tpu;
   pl->deep = ctx_blocks <= compute_units() ? 1 : 0;
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(uint32_t));
@@ -158,6 +167,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.max_ctx_len = bt->max_ctx_len; p.max_questions = bt->max_questions;
   p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
   p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.ctx_blocks = pl.ctx_blocks;
+  p.seg_tpu = pl.seg_tpu;
   // merge: enough threads per item that each folds at most 8 of the
   // max_chunks + 1 partial states; items split over workgroups of 512
   {
@@ -286,6 +296,6 @@ const char* ippd_status_string(ippd_status_t s) {
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 300; }
+int ippd_version(void) { return 400; }
 
 }  // extern "C"

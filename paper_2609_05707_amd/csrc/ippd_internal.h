@@ -37,20 +37,22 @@ struct AppendParams {
   double inv_freq[kMaxHalfDim];
 };
 
-// Launch plan of one decode call (attend_kernel + merge_kernel).  A
-// group is (prompt b, kv head g) for IPPD or (question i, kv head g) for the
-// standard baseline; a context unit is (group, chunk, row group) with
-// 16*waves query rows.
+// Launch plan of one decode call (attend_kernel + merge_kernel).  A group is
+// (prompt b, kv head g) for IPPD or (question i, kv head g) for the standard
+// baseline; a context unit is (group, chunk, row group) with 16*waves query
+// rows; a segment unit serves seg_tpu tasks (question i, kv head g).
 struct StepPlan {
   int shared;              // 1: IPPD, context units serve all questions of a prompt
-  int waves;               // waves per context unit
+  int waves;               // waves per workgroup; a context unit covers 16 rows per wave
   int nrg;                 // row groups per group
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
   int n_groups;
-  int grid;                // attend_kernel workgroups: context units, then segment units
+  int grid;                // attend_kernel workgroups: ctx_blocks + seg_blocks
   int ctx_blocks;          // context units (8 * nrg * ceil(n_groups * max_chunks / 8))
-  int deep;                // 1: deep LDS ring (grid fits the chip in one wave)
+  int seg_blocks;          // segment units: ceil(Nt * Hkv / seg_tpu)
+  int seg_tpu;             // segment tasks per unit (power of two dividing waves)
+  int deep;                // 1: deep LDS ring (the context units fit the chip in one wave)
   size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states (chunks, segment)
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
   size_t workspace_bytes;
@@ -64,12 +66,12 @@ struct StepParams {
   const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   float* out; float* lse;
-  uint32_t* counters;      // [Nt] per-question arrivals of the fused step (zero between calls)
+  uint32_t* counters;      // [Nt] per-question arrivals of the fused step's merge (zero between calls)
   float* part_acc;         // [part_slots][D]
   float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
-  int shared, fused, nrg, chunk, max_chunks, n_groups, ctx_blocks;
+  int shared, fused, nrg, chunk, max_chunks, n_groups, ctx_blocks, seg_tpu;
   int merge_phases;        // threads per merged item (slots split among them), power of 2
   int merge_parts;         // merge workgroups per question
   float c;                 // scale * log2(e)

@@ -94,7 +94,7 @@ def oracle_steps(st: W.Structure, kv: W.LayerKV, steps: Iterable[int], record: S
 
 def bookkeeping_zero(db: DecodeBatch) -> bool:
     """The per-question merge bookkeeping at the head of both workspaces (Nt
-    int32) is back at zero after every call."""
+    uint32) is back at zero after every call."""
     torch.cuda.synchronize()
     return bool(torch.all(db.ws_ippd[: 4 * db.Nt] == 0)) and bool(torch.all(db.ws_std[: 4 * db.Nt] == 0))
 
