@@ -261,31 +261,40 @@ __device__ __forceinline__ void mask_scores(f32x4_t (&sc)[2], int n, int lg) {
     for (int v = 0; v < 4; ++v) sc[kb][v] = 8 * lg + 4 * kb + v >= n ? -INFINITY : sc[kb][v];
 }
 
-// One ring tile for one 16-row block.  n = valid tokens of the tile (32 except
-// for the chunk's last tile).
-template <typename T, int D, int NS>
-__device__ __forceinline__ void ring_tile(const unsigned char* stage, const typename Mfma<T>::Frag (&qf)[D / 32],
-                                          RowState<D>& st, int n, int lr, int lg, float c) {
+// One ring tile for RB 16-row blocks of one wave: every K and V fragment is
+// read from LDS once and used by all RB blocks.  n = valid tokens of the tile
+// (32 except for the chunk's last tile).
+template <typename T, int D, int NS, int RB>
+__device__ __forceinline__ void ring_tile(const unsigned char* stage, const typename Mfma<T>::Frag (&qf)[RB][D / 32],
+                                          RowState<D> (&st)[RB], int n, int lr, int lg, float c) {
   using R = Ring<T, D, NS>;
   using M = Mfma<T>;
   constexpr int DS = D / 32;
-  f32x4_t sc[2];
+  f32x4_t sc[RB][2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const int r = 16 * kb + lr;
     const int sw = (r >> R::KSH) & R::KMASK;
     const unsigned char* row = stage + r * (R::CPR * 16);
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) {
       const int c0 = (8 * lg + 32 * ds) * R::E / 16;        // logical chunk of this fragment
       const typename M::Frag kf = M::lds2(row + ((c0 ^ sw) * 16), row + (((c0 + 1) ^ sw) * 16));
-      acc = M::mma(kf, qf[ds], acc);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb] = M::mma(kf, qf[rb][ds], acc[rb]);
     }
-    sc[kb] = acc;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) sc[rb][kb] = acc[rb];
   }
-  if (n < 32) mask_scores(sc, n, lg);
-  const typename M::Frag pf = softmax_step<T, D>(sc, st, c);
+  typename M::Frag pf[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (n < 32) mask_scores(sc[rb], n, lg);
+    pf[rb] = softmax_step<T, D>(sc[rb], st[rb], c);
+  }
   const int keep = min(max(n - 8 * lg, 0), 8);
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
@@ -293,7 +302,8 @@ __device__ __forceinline__ void ring_tile(const unsigned char* stage, const type
     const unsigned char* vp = stage + R::KBYTES + lg * R::VBLK + (16 * db + lr) * 8 * R::E;
     typename M::Frag vf = M::lds2(vp, vp + 16);
     if (n < 32) vf = M::keep_first(vf, keep);                // never NaN * 0 past the end
-    st.o[db] = M::mma(vf, pf, st.o[db]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st[rb].o[db] = M::mma(vf, pf[rb], st[rb].o[db]);
   }
 }
 
@@ -388,28 +398,33 @@ __device__ __forceinline__ u32x4_t gload_b128(const void* p) {
   return r;
 }
 
-template <typename T, int D, bool FUSED>
+template <typename T, int D, bool FUSED, int RB>
 struct RowLoads {
-  static constexpr int QN = D * static_cast<int>(sizeof(T)) / 64;   // 16-byte query pieces per lane
+  static constexpr int QN = D * static_cast<int>(sizeof(T)) / 64;   // 16-byte query pieces per lane and row
   static constexpr int QPF = static_cast<int>(sizeof(T)) / 2;       // pieces per 8-element fragment
   static constexpr int TN = FUSED ? D / 16 : 0;                    // 16-byte pieces of the lane's D/8 frequencies
-  uint32_t a, s;
-  u32x4_t q[QN];
+  uint32_t a[RB], s[RB];
+  u32x4_t q[RB][QN];
   u32x4_t th[TN > 0 ? TN : 1];
 };
 
-// Lane (lg, lr) of row (question qi, head h): dims 32*ds + 8*lg + u of the
-// query (raw q_new in the fused step, rotated q_rot_in otherwise).
-template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void issue_row_loads(RowLoads<T, D, FUSED>& r, const StepParams& p, int qi, int h, int lg) {
-  using RL = RowLoads<T, D, FUSED>;
-  r.a = gload_u8(p.active + qi);
-  r.s = gload_b32(p.seg_len + qi);
-  const char* src = static_cast<const char*>(FUSED ? p.q_new : p.q_rot_in) +
-                    ((static_cast<int64_t>(qi) * p.Hq + h) * D + lg * 8) * static_cast<int64_t>(sizeof(T));
+// Lane (lg, lr) of row block rb (question qi[rb], head h[rb]): dims
+// 32*ds + 8*lg + u of the query (raw q_new in the fused step, rotated
+// q_rot_in otherwise).
+template <typename T, int D, bool FUSED, int RB>
+__device__ __forceinline__ void issue_row_loads(RowLoads<T, D, FUSED, RB>& r, const StepParams& p, const int (&qi)[RB],
+                                                const int (&h)[RB], int lg) {
+  using RL = RowLoads<T, D, FUSED, RB>;
 #pragma unroll
-  for (int k = 0; k < RL::QN; ++k)
-    r.q[k] = gload_b128(src + (k / RL::QPF) * 32 * static_cast<int>(sizeof(T)) + (k % RL::QPF) * 16);
+  for (int rb = 0; rb < RB; ++rb) {
+    r.a[rb] = gload_u8(p.active + qi[rb]);
+    r.s[rb] = gload_b32(p.seg_len + qi[rb]);
+    const char* src = static_cast<const char*>(FUSED ? p.q_new : p.q_rot_in) +
+                      ((static_cast<int64_t>(qi[rb]) * p.Hq + h[rb]) * D + lg * 8) * static_cast<int64_t>(sizeof(T));
+#pragma unroll
+    for (int k = 0; k < RL::QN; ++k)
+      r.q[rb][k] = gload_b128(src + (k / RL::QPF) * 32 * static_cast<int>(sizeof(T)) + (k % RL::QPF) * 16);
+  }
   if constexpr (FUSED) {
     // theta of pairs 32*ds + 8*lg + u, u = 0..7: 64 contiguous bytes per ds,
     // read where the launch placed StepParams (the kernel's only argument)
@@ -420,37 +435,38 @@ __device__ __forceinline__ void issue_row_loads(RowLoads<T, D, FUSED>& r, const 
   }
 }
 
-template <int N, typename T, int D, bool FUSED>
-__device__ __forceinline__ void wait_row_loads(RowLoads<T, D, FUSED>& r) {
+// The one wait for the row loads: s_waitcnt vmcnt(N), then every destination
+// register is tied to an asm statement at that point, so that none is read
+// (or copied) before it (volatile asm statements keep their order).
+template <int N, typename T, int D, bool FUSED, int RB>
+__device__ __forceinline__ void wait_row_loads(RowLoads<T, D, FUSED, RB>& r) {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  using RL = RowLoads<T, D, FUSED>;
-  static_assert(RL::QN == 2 || RL::QN == 4 || RL::QN == 8, "query pieces");
-  static_assert(RL::TN == 0 || RL::TN == 4 || RL::TN == 8, "frequency pieces");
-  if constexpr (RL::QN == 2) {
-    asm volatile("s_waitcnt vmcnt(%4)" : "+v"(r.a), "+v"(r.s), "+v"(r.q[0]), "+v"(r.q[1]) : "n"(N));
-  } else {
-    asm volatile("s_waitcnt vmcnt(%6)"
-                 : "+v"(r.a), "+v"(r.s), "+v"(r.q[0]), "+v"(r.q[1]), "+v"(r.q[2]), "+v"(r.q[3])
-                 : "n"(N));
-    if constexpr (RL::QN == 8) asm volatile("" : "+v"(r.q[4]), "+v"(r.q[5]), "+v"(r.q[6]), "+v"(r.q[7]));
+  using RL = RowLoads<T, D, FUSED, RB>;
+  asm volatile("s_waitcnt vmcnt(%2)" : "+v"(r.a[0]), "+v"(r.s[0]) : "n"(N));
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (rb > 0) asm volatile("" : "+v"(r.a[rb]), "+v"(r.s[rb]));
+#pragma unroll
+    for (int k = 0; k < RL::QN; ++k) asm volatile("" : "+v"(r.q[rb][k]));
   }
-  if constexpr (RL::TN >= 4) asm volatile("" : "+v"(r.th[0]), "+v"(r.th[1]), "+v"(r.th[2]), "+v"(r.th[3]));
-  if constexpr (RL::TN == 8) asm volatile("" : "+v"(r.th[4]), "+v"(r.th[5]), "+v"(r.th[6]), "+v"(r.th[7]));
+#pragma unroll
+  for (int k = 0; k < RL::TN; ++k) asm volatile("" : "+v"(r.th[k]));
 }
 
-// Query fragments (B operand) from the row loads, rotated at pos in the
-// fused step.  Pair j < D/2 is (x_j, x_{j+D/2}): fragments ds and ds + DS/2.
-template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], const RowLoads<T, D, FUSED>& r,
-                                          int64_t pos) {
+// Query fragments (B operand) of one row block from its loaded pieces,
+// rotated at pos in the fused step.  Pair j < D/2 is (x_j, x_{j+D/2}):
+// fragments ds and ds + DS/2.
+template <typename T, int D, bool FUSED, int QN, int TN>
+__device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], const u32x4_t (&q)[QN],
+                                          const u32x4_t (&th)[TN], int64_t pos) {
   using M = Mfma<T>;
   constexpr int DS = D / 32;
 #pragma unroll
   for (int ds = 0; ds < DS; ++ds) {
     if constexpr (sizeof(T) == 2) {
-      qf[ds] = __builtin_bit_cast(typename M::Frag, r.q[ds]);
+      qf[ds] = __builtin_bit_cast(typename M::Frag, q[ds]);
     } else {
-      const f32x4_t x = __builtin_bit_cast(f32x4_t, r.q[2 * ds]), y = __builtin_bit_cast(f32x4_t, r.q[2 * ds + 1]);
+      const f32x4_t x = __builtin_bit_cast(f32x4_t, q[2 * ds]), y = __builtin_bit_cast(f32x4_t, q[2 * ds + 1]);
       qf[ds] = typename M::Frag{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
     }
   }
@@ -461,7 +477,7 @@ __device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], 
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       float cs, sn, xr, yr;
-      const u32x4_t tp = r.th[4 * ds + u / 2];
+      const u32x4_t tp = th[4 * ds + u / 2];
       const double theta = __hiloint2double(static_cast<int>(tp[2 * (u & 1) + 1]), static_cast<int>(tp[2 * (u & 1)]));
       rope_cos_sin(pos, theta, cs, sn);
       rope_rotate(x[u], y[u], cs, sn, xr, yr);
@@ -501,11 +517,12 @@ struct UnitLds {
 // its tiles through that XCD's L2) and chunks are dealt to the slices round
 // robin.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW, int NS, bool FUSED>
+template <typename T, int D, int NW, int NS, bool FUSED, int RB>
 __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char* ring, int wave, int lane) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
-  constexpr int RW = 16 * NW, DPT = RG::BLOCKS / NW;
+  using RL = RowLoads<T, D, FUSED, RB>;
+  constexpr int RW = 16 * RB * NW, DPT = RG::BLOCKS / NW;
   constexpr int P0 = RG::NS - 1 < 3 ? RG::NS - 1 : 3;      // tiles issued before the queries are rotated
   const int lr = lane & 15, lg = lane >> 4;
   const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
@@ -551,13 +568,20 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
   const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-  // this lane's row: question qa + row / G, head g*G + row % G
-  const int row = row0 + 16 * wave + lr;
-  const bool in_range = row < nrows;
-  const int rr = in_range ? row : nrows - 1;
-  const int qi = qa + rr / G, h = g * G + rr % G;
-  RowLoads<T, D, FUSED> rl;
-  issue_row_loads<T, D, FUSED>(rl, p, qi, h, lg);
+  // this lane's rows: row block rb of wave w holds rows 16*(RB*w + rb) + lr
+  // of the unit, row r being question qa + r / G, head g*G + r % G
+  int qi[RB], h[RB];
+  bool in_range[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = row0 + 16 * (RB * wave + rb) + lr;
+    in_range[rb] = row < nrows;
+    const int rr = in_range[rb] ? row : nrows - 1;
+    qi[rb] = qa + rr / G;
+    h[rb] = g * G + rr % G;
+  }
+  RL rl;
+  issue_row_loads<T, D, FUSED, RB>(rl, p, qi, h, lg);
   // exactly P0 tiles go out before the one wait for the row loads (a unit
   // with fewer tiles fetches its last tile again): a single wait with a
   // fixed count leaves the compiler no reason to copy the loaded registers
@@ -568,20 +592,28 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
   wait_row_loads<(P0 * DPT < 63 ? P0 * DPT : 63)>(rl);
 
-  const int s_raw = static_cast<int>(rl.s);
-  const bool act = in_range && rl.a != 0u && usable_seg_len(p, s_raw) >= 0;
-  const bool live = __any(act);                    // wave-uniform
-  typename M::Frag qf[D / 32];
-  row_query<T, D, FUSED>(qf, rl, static_cast<int64_t>(ctx_len) + s_raw);
-  if (!act) {
+  bool act[RB];
+  bool any_act = false;
+  typename M::Frag qf[RB][D / 32];
 #pragma unroll
-    for (int ds = 0; ds < D / 32; ++ds) qf[ds] = M::zero();
+  for (int rb = 0; rb < RB; ++rb) {
+    const int s_raw = static_cast<int>(rl.s[rb]);
+    act[rb] = in_range[rb] && rl.a[rb] != 0u && usable_seg_len(p, s_raw) >= 0;
+    any_act = any_act || act[rb];
+    row_query<T, D, FUSED, RL::QN, (RL::TN > 0 ? RL::TN : 1)>(qf[rb], rl.q[rb], rl.th,
+                                                              static_cast<int64_t>(ctx_len) + s_raw);
+    if (!act[rb]) {
+#pragma unroll
+      for (int ds = 0; ds < D / 32; ++ds) qf[rb][ds] = M::zero();
+    }
   }
+  const bool live = __any(any_act);                // wave-uniform
 #pragma unroll
   for (int t = P0; t < RG::NS - 1; ++t)
     if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane);
-  RowState<D> st;
-  row_init(st);
+  RowState<D> st[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) row_init(st[rb]);
   const float c = p.c;
 
   // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
@@ -596,13 +628,16 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     const int tn = t + RG::NS - 1;
     if (tn <= last)
       issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane);
-    if (live) ring_tile<T, D, NS>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+    if (live) ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
   }
   wait_vmcnt<0>();                                  // no LDS-DMA may outlive the workgroup
 
-  float l = xor16_sum(st.l);
-  st.l = xor32_sum(l);
-  if (act) publish_rows<D>(p, st, (static_cast<int64_t>(chunk) * p.Nt + qi) * p.Hq + h, lg);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float l = xor16_sum(st[rb].l);
+    st[rb].l = xor32_sum(l);
+    if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(chunk) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -851,13 +886,15 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
 // Workgroups are dispatched in order, so segment units start as context
 // units retire and fill the tail of the context work.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW, int NS, bool FUSED>
-__global__ __launch_bounds__(64 * NW, 4) void attend_kernel(StepParams p) {
+// RB = 1: four waves per SIMD (two workgroups per compute unit); RB = 2
+// carries twice the accumulators, at two waves per SIMD.
+template <typename T, int D, int NW, int NS, bool FUSED, int RB>
+__global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepParams p) {
   __shared__ UnitLds<T, D, NW, NS> sh;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int blk = static_cast<int>(blockIdx.x);
-  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED>(p, sh.main, wave, lane);
+  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
   else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks, wave, lane);
 }
 
@@ -967,49 +1004,58 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW, int NS>
+template <typename T, int D, int NW, int NS, int RB>
 static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
-  if (p.fused) attend_kernel<T, D, NW, NS, true><<<grid, 64 * NW, 0, s>>>(p);
-  else attend_kernel<T, D, NW, NS, false><<<grid, 64 * NW, 0, s>>>(p);
+  if (p.fused) attend_kernel<T, D, NW, NS, true, RB><<<grid, 64 * NW, 0, s>>>(p);
+  else attend_kernel<T, D, NW, NS, false, RB><<<grid, 64 * NW, 0, s>>>(p);
   return hipGetLastError();
 }
 
 // Ring depth: 4 stages (two workgroups per CU) in general; 8 (one per CU,
 // every tile of a short unit in flight at once) when the context units fit
-// the chip in one wave.  fp32 at D = 128 has 32 KB stages: 2 or 4.
-template <typename T, int D, int NW>
+// the chip in one wave, or when registers allow one workgroup per CU anyway.
+// fp32 at D = 128 has 32 KB stages: 2 or 4.
+template <typename T, int D, int NW, int RB>
 static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStream_t s) {
   constexpr int base = (2 * 32 * D * sizeof(T)) > 16384 ? 2 : 4;
-  return deep ? launch_attend<T, D, NW, 2 * base>(grid, p, s) : launch_attend<T, D, NW, base>(grid, p, s);
+  return deep ? launch_attend<T, D, NW, 2 * base, RB>(grid, p, s) : launch_attend<T, D, NW, base, RB>(grid, p, s);
 }
 
 template <typename T, int D>
-static hipError_t launch_waves(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+static hipError_t launch_waves(int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  if (rb == 2) {
+    // two row blocks per wave: bf16 at D = 128 with four or eight waves
+    if constexpr (sizeof(T) == 2 && D == 128) {
+      if (waves == 4) return launch_depth<T, D, 4, 2>(deep, grid, p, s);
+      if (waves == 8) return launch_depth<T, D, 8, 2>(deep, grid, p, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (waves) {
-    case 1: return launch_depth<T, D, 1>(deep, grid, p, s);
-    case 2: return launch_depth<T, D, 2>(deep, grid, p, s);
-    case 4: return launch_depth<T, D, 4>(deep, grid, p, s);
+    case 1: return launch_depth<T, D, 1, 1>(deep, grid, p, s);
+    case 2: return launch_depth<T, D, 2, 1>(deep, grid, p, s);
+    case 4: return launch_depth<T, D, 4, 1>(deep, grid, p, s);
     default:
       // the planner gives fp32 at D = 128 at most four waves
       if constexpr (sizeof(T) == 4 && D == 128) return hipErrorInvalidValue;
-      else return launch_depth<T, D, 8>(deep, grid, p, s);
+      else return launch_depth<T, D, 8, 1>(deep, grid, p, s);
   }
 }
 
 template <typename T, int D>
-static hipError_t launch_d(int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
-  hipError_t e = launch_waves<T, D>(waves, deep, grid, p, s);
+static hipError_t launch_d(int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  hipError_t e = launch_waves<T, D>(waves, rb, deep, grid, p, s);
   if (e != hipSuccess) return e;
   merge_kernel<D><<<static_cast<unsigned>(p.Nt) * p.merge_parts, kMergeThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
-hipError_t launch_step(int dtype, int waves, bool deep, int grid, const StepParams& p, hipStream_t s) {
+hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
   if (p.Nt == 0 || grid == 0) return hipSuccess;
   if (dtype == 0)
-    return p.D == 64 ? launch_d<float, 64>(waves, deep, grid, p, s) : launch_d<float, 128>(waves, deep, grid, p, s);
-  return p.D == 64 ? launch_d<uint16_t, 64>(waves, deep, grid, p, s)
-                   : launch_d<uint16_t, 128>(waves, deep, grid, p, s);
+    return p.D == 64 ? launch_d<float, 64>(waves, rb, deep, grid, p, s) : launch_d<float, 128>(waves, rb, deep, grid, p, s);
+  return p.D == 64 ? launch_d<uint16_t, 64>(waves, rb, deep, grid, p, s)
+                   : launch_d<uint16_t, 128>(waves, rb, deep, grid, p, s);
 }
 
 }  // namespace ippd

@@ -11,7 +11,6 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
-constexpr int kTargetUnits = 512;    // context units aimed for per launch (2 resident per CU)
 constexpr int kMinChunk = 256;
 constexpr int kMaxChunk = 4096;
 
@@ -32,8 +31,9 @@ ippd_status_t check_batch(const ippd_batch_t* bt) {
   if (bt->max_questions < 1 || bt->max_questions > ippd::kMaxQuestionsPerPrompt) return IPPD_ERR_SHAPE;
   if (bt->chunk_tokens < 0 || (bt->chunk_tokens & 31)) return IPPD_ERR_SHAPE;
   if (bt->tile_rows != 0 && bt->tile_rows != 16 && bt->tile_rows != 32 && bt->tile_rows != 64 &&
-      bt->tile_rows != 128)
+      bt->tile_rows != 128 && bt->tile_rows != 256)
     return IPPD_ERR_SHAPE;
+  if (bt->tile_rows == 256 && !(bt->dtype == IPPD_DTYPE_BF16 && bt->head_dim == 128)) return IPPD_ERR_SHAPE;
   if (!(bt->rope_base > 0.0) || !isfinite(bt->rope_base)) return IPPD_ERR_SHAPE;
   if (!isfinite(bt->scale)) return IPPD_ERR_SHAPE;
   if (!bt->ctx_off || !bt->ctx_len || !bt->q_start || !bt->seg_len || !bt->active || !bt->err_flag)
@@ -74,18 +74,27 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   if (check_batch(bt) != IPPD_OK) return false;
   const int G = bt->num_q_heads / bt->num_kv_heads;
   const int64_t max_rows = shared ? static_cast<int64_t>(bt->max_questions) * G : G;
-  // waves per workgroup; a context unit covers 16 rows per wave
-  int waves = bt->tile_rows / 16;
-  if (waves == 0) waves = max_rows <= 16 ? 1 : (max_rows <= 32 ? 2 : (max_rows <= 64 ? 4 : 8));
+  // rows per context unit: 16 * rb per wave.  bf16 at D = 128 with more than
+  // 64 rows puts two 16-row blocks on each wave (each K/V fragment read from
+  // LDS serves both): 128 rows as 4 x 32, 256 as 8 x 32.
+  const bool two_blocks_ok = bt->dtype == IPPD_DTYPE_BF16 && bt->head_dim == 128;
+  int rows = bt->tile_rows;
+  if (rows == 0) rows = max_rows <= 16 ? 16 : (max_rows <= 32 ? 32 : (max_rows <= 64 ? 64 : (max_rows <= 128 || !two_blocks_ok ? 128 : 256)));
+  int rb = rows > 64 && two_blocks_ok ? 2 : 1;
+  int waves = rows / (16 * rb);
   // fp32 at D = 128: the operands of eight waves do not fit their registers
   if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && waves > 4) waves = 4;
-  const int nrg = static_cast<int>((max_rows + 16 * waves - 1) / (16 * waves));
+  const int nrg = static_cast<int>((max_rows + 16 * rb * waves - 1) / (16 * rb * waves));
+  // workgroups resident per compute unit (eight waves of two row blocks use
+  // the registers of two)
+  const int wg_per_cu = (rb == 2 && waves == 8) ? 1 : 2;
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   int chunk = bt->chunk_tokens;
   if (chunk == 0) {
     const int64_t work = n_groups * nrg * bt->max_ctx_len;
-    int64_t ch = (work + kTargetUnits - 1) / kTargetUnits;
+    const int64_t target = static_cast<int64_t>(compute_units()) * wg_per_cu;
+    int64_t ch = (work + target - 1) / target;
     ch = (ch + 31) / 32 * 32;
     ch = ch < kMinChunk ? kMinChunk : (ch > kMaxChunk ? kMaxChunk : ch);
     chunk = static_cast<int>(ch);
@@ -104,6 +113,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
+  pl->rb = rb;
   pl->nrg = nrg;
   pl->chunk = chunk;
   pl->max_chunks = static_cast<int>(max_chunks);
@@ -112,7 +122,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->ctx_blocks = static_cast<int>(ctx_blocks);
   pl->seg_blocks = static_cast<int>(seg_blocks);
   pl->seg_tpu = tpu;
-  pl->deep = ctx_blocks <= compute_units() ? 1 : 0;
+  pl->deep = (ctx_blocks <= compute_units() || wg_per_cu == 1) ? 1 : 0;
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(uint32_t));
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
@@ -181,7 +191,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
-  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.deep != 0, pl.grid, p, stream));
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));
 }
 
 }  // namespace

@@ -43,7 +43,8 @@ struct AppendParams {
 // rows; a segment unit serves seg_tpu tasks (question i, kv head g).
 struct StepPlan {
   int shared;              // 1: IPPD, context units serve all questions of a prompt
-  int waves;               // waves per workgroup; a context unit covers 16 rows per wave
+  int waves;               // waves per workgroup; a context unit covers 16 * rb rows per wave
+  int rb;                  // 16-row blocks per wave (1, or 2 for bf16 at D = 128)
   int nrg;                 // row groups per group
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
@@ -82,6 +83,6 @@ struct StepParams {
 hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s);
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
-hipError_t launch_step(int dtype, int waves, bool deep, int grid, const StepParams& p, hipStream_t s);
+hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s);
 
 }  // namespace ippd

@@ -193,14 +193,15 @@ def test_empty_context_and_many_questions():
 
 @pytest.mark.parametrize("fused", [False, True])
 def test_group_of_three_heads(fused):
-    """G = 3 query heads per kv head: a 16-row tile boundary falls inside a question."""
+    """G = 3 query heads per kv head: a 16-row tile boundary falls inside a question
+    (rows per context unit 16..256; 128 and 256 put two 16-row blocks on a wave)."""
     log(f"case: G=3 (Hq 6, Hkv 2) fused={fused}")
     wl = W.custom_workload(wid=240, dtype="bf16", num_prompts=2, hq=6, hkv=2, head_dim=128,
                            ctx_len=(90, 300), questions=(7, 13), seg_len=(2, 30), steps=2,
                            value_std=0.5)
     st = W.make_structure(wl)
     kv = W.layer_kv(st)
-    for rows in (16, 32, 64):
+    for rows in (16, 32, 64, 128, 256):
         gpu = run_gpu(st, [0, 1], [0, 1], kv=kv, fused=fused, tile_rows=rows, chunk_tokens=64)
         ref = oracle_steps(st, kv, [0, 1], [0, 1])
         assert gpu.err == 0
