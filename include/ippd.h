@@ -158,15 +158,15 @@ ippd_status_t ippd_append_kv(const ippd_batch_t *batch, const void *q_new,
                              const ippd_kv_cache_t *kv, hipStream_t stream);
 
 /*
- * Workspace of the decode calls: device scratch holding one arrival counter
- * per question and the partial softmax states (max, sum, weighted values) of
- * the context chunks and segments.  ippd_decode_workspace_bytes serves
+ * Workspace of the decode calls: device scratch holding the partial softmax
+ * states (max, sum, weighted values) of every (context chunk, question, head)
+ * and (segment, question, head).  ippd_decode_workspace_bytes serves
  * ippd_decode_attention and ippd_decode_step, standard_decode_workspace_bytes
  * the two standard_* calls (sizes depend only on host-side fields; 0 means an
- * invalid batch).  A workspace must be 256-byte aligned and ZERO-FILLED
- * before its first use; every call leaves its counters at zero again, so it
- * can be reused by later calls on the same stream without clearing.  Calls
- * that run concurrently need separate workspaces.
+ * invalid batch).  A workspace must be 256-byte aligned.  It needs no
+ * initialisation and carries nothing from one call to the next: every state
+ * a call reads was written earlier in the same call.  Calls that run
+ * concurrently need separate workspaces.
  */
 size_t ippd_decode_workspace_bytes(const ippd_batch_t *batch);
 size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);

@@ -558,7 +558,22 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   const int nrows = (qb - qa) * G;
   const int row0 = rg * RW;
   const int ctx_len = p.ctx_len[b];
-  if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len || row0 >= nrows) return;
+  if (row0 >= nrows) return;
+  if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len) {
+    // past the prompt's context: an empty state (max -inf) for each row, so
+    // that the merge can fold every chunk slot without knowing the prompt
+    if (lg == 0) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = row0 + 16 * (RB * wave + rb) + lr;
+        if (row < nrows) {
+          const int64_t slot = (static_cast<int64_t>(chunk) * p.Nt + qa + row / G) * p.Hq + g * G + row % G;
+          *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, 0.f);
+        }
+      }
+    }
+    return;
+  }
 
   const int64_t off = p.ctx_off[b];
   const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
@@ -847,11 +862,21 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   }
   __syncthreads();
   // combine each task's wave states and its last key: item (task, row r, dims d0..d0+7)
+  // a task that is not served marks its rows skipped (sum -1), so the merge
+  // needs no question metadata
   const int per_task = G * (D / 8);
   for (int e = threadIdx.x; e < tpu * per_task; e += 64 * NW) {
     const int kk = e / per_task, er = e - kk * per_task;
-    if (!sh.live[kk]) continue;
     const int r = er / (D / 8), d0 = (er - r * (D / 8)) * 8;
+    if (!sh.live[kk]) {
+      const int tk = u * tpu + kk;
+      if (d0 == 0 && tk < p.Nt * p.Hkv) {
+        const int ik = tk / p.Hkv, gk = tk - ik * p.Hkv;
+        const int64_t slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + ik) * p.Hq + gk * G + r;
+        *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, -1.f);
+      }
+      continue;
+    }
     const float sl = sh.slast[kk][r];
     float m = sl;
     for (int w = 0; w < sw; ++w) m = fmaxf(m, sh.ml[kk * sw + w][r].x);
@@ -901,16 +926,22 @@ __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepPa
 // ---------------------------------------------------------------------------
 // merge_kernel: question i is served by merge_parts workgroups of
 // kMergeThreads threads.  Item (head h, dims d0..d0+7) of the question
-// combines its context chunks and its segment state:
+// combines its context chunk states and its segment state:
 //   m = max_k m_k,  l = sum_k 2^(c(m_k - m)) l_k,  o = sum_k 2^(c(m_k - m)) o_k / l.
 // With P = merge_phases, a workgroup takes kMergeThreads / P items and P
 // threads per item, thread phase f folding slots f, f + P, ...; the P states
-// of an item are then combined through LDS.
+// of an item are then combined through LDS.  Every slot of every question
+// is written by the attend kernel (chunks past a prompt's context hold an
+// empty state, the segment slot of a question not served holds sum -1), so
+// one round of loads brings all the kernel reads, with no question
+// metadata; only part 0 of a question reads its segment length, and
+// advances it in the fused step.
 // ---------------------------------------------------------------------------
 constexpr int kMergeThreads = 512;
 constexpr int kMergeBatch = 8;       // partial states in flight per thread
 
-// Exact combination of partial softmax states (m, l, a) in 2^(c*x) units.
+// Exact combination of partial softmax states (m, l, a) in 2^(c*x) units;
+// an empty state (m = -inf) changes nothing.
 struct MergeAcc {
   float m, l;
   f32x4_t a0, a1;
@@ -921,10 +952,10 @@ struct MergeAcc {
     a1 = a0;
   }
   __device__ __forceinline__ void fold(float mk, float lk, f32x4_t x0, f32x4_t x1, float c) {
+    if (mk == -INFINITY) return;
     const float mn = fmaxf(m, mk);
-    const float ms = mn == -INFINITY ? 0.f : mn;
-    const float sa = fast_exp2((m - ms) * c);        // 0 while m = -inf
-    const float sb = fast_exp2((mk - ms) * c);
+    const float sa = fast_exp2((m - mn) * c);        // 0 while m = -inf
+    const float sb = fast_exp2((mk - mn) * c);
     l = l * sa + sb * lk;
     a0 = a0 * sa + x0 * sb;
     a1 = a1 * sa + x1 * sb;
@@ -935,21 +966,19 @@ struct MergeAcc {
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
   __shared__ __attribute__((aligned(16))) float mp[kMergeThreads * 12];   // (m, l, -, -, 8 values) per thread
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x;
   const int P = p.merge_phases, per = kMergeThreads / P;
   const int i = blockIdx.x / p.merge_parts, part = blockIdx.x - i * p.merge_parts;
-  const PromptInfo pi = find_prompt(p, i, lane);
-  const bool act = p.active[i] != 0;
-  const int s = usable_seg_len(p, p.seg_len[i]);
-  if (!act || s < 0 || !pi.ok) return;             // workgroup-uniform; flagged elsewhere
-  const int nc = min((pi.len + p.chunk - 1) / p.chunk, p.max_chunks);
-  const int nslot = nc + 1;                        // chunks, then the segment
+  const int nslot = p.max_chunks + 1;              // chunks, then the segment
   const float c = p.c;
   const int items = p.Hq * (D / 8);
   const int f = tid / per, local = tid - f * per;
   const int e = part * per + local;                // this thread's item
   const bool has = e < items;
   const int h = has ? e / (D / 8) : 0, d0 = has ? (e - h * (D / 8)) * 8 : 0;
+  const int64_t seg_slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + i) * p.Hq + h;
+  const float seg_l = p.part_ml[2 * seg_slot + 1];
+  const int s = (p.fused && part == 0 && tid == 0) ? p.seg_len[i] : 0;
   MergeAcc acc;
   acc.init();
   for (int k0 = f; k0 < nslot; k0 += P * kMergeBatch) {
@@ -957,8 +986,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
     f32x4_t x0[kMergeBatch], x1[kMergeBatch];
 #pragma unroll
     for (int uu = 0; uu < kMergeBatch; ++uu) {
-      const int k = min(k0 + P * uu, nslot - 1);
-      const int ck = k < nc ? k : p.max_chunks;
+      const int ck = min(k0 + P * uu, nslot - 1);
       const int64_t slot = (static_cast<int64_t>(ck) * p.Nt + i) * p.Hq + h;
       ml[uu] = *reinterpret_cast<const float2*>(p.part_ml + 2 * slot);
       const f32x4_t* src = reinterpret_cast<const f32x4_t*>(p.part_acc + slot * D + d0);
@@ -969,6 +997,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
     for (int uu = 0; uu < kMergeBatch; ++uu)
       if (k0 + P * uu < nslot) acc.fold(ml[uu].x, ml[uu].y, x0[uu], x1[uu], c);
   }
+  // every head's segment slot of question i carries the same served/skipped
+  // mark, so the decision is workgroup-uniform
+  if (seg_l < 0.f) return;
   if (P > 1) {
     float* dst = mp + tid * 12;
     dst[0] = acc.m;
@@ -990,17 +1021,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
     dst[1] = acc.a1 * inv;
     if (p.lse != nullptr && d0 == 0) p.lse[static_cast<int64_t>(i) * p.Hq + h] = acc.m * p.scale + logf(acc.l);
   }
-  if (p.fused) {
-    // every thread of the workgroup has read seg_len[i] above; with several
-    // workgroups per question the last one to arrive advances it
-    __syncthreads();
-    if (tid == 0) {
-      if (p.merge_parts == 1 || atomicAdd(p.counters + i, 1u) == static_cast<uint32_t>(p.merge_parts - 1)) {
-        if (p.merge_parts > 1) p.counters[i] = 0;
-        p.seg_len[i] = s + 1;
-      }
-    }
-  }
+  // the question was served: its segment holds the step's token
+  if (p.fused && part == 0 && tid == 0) p.seg_len[i] = s + 1;
 }
 
 // ---------------------------------------------------------------------------

@@ -124,7 +124,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->seg_tpu = tpu;
   pl->deep = (ctx_blocks <= compute_units() || wg_per_cu == 1) ? 1 : 0;
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
-  pl->off_acc = round256(static_cast<size_t>(bt->num_questions) * sizeof(uint32_t));
+  pl->off_acc = 0;
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
   return true;
@@ -168,7 +168,6 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.seg_len = bt->seg_len; p.active = bt->active; p.err_flag = bt->err_flag;
   p.out = out; p.lse = lse;
   char* ws = static_cast<char*>(workspace);
-  p.counters = reinterpret_cast<uint32_t*>(ws);
   p.part_acc = reinterpret_cast<float*>(ws + pl.off_acc);
   p.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   p.pool = bt->ctx_pool_tokens;

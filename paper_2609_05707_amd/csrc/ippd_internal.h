@@ -67,7 +67,6 @@ struct StepParams {
   const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
   float* out; float* lse;
-  uint32_t* counters;      // [Nt] per-question arrivals of the fused step's merge (zero between calls)
   float* part_acc;         // [part_slots][D]
   float* part_ml;          // [part_slots][2]: running max (raw logit units), sum
   int64_t pool;

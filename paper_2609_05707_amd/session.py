@@ -100,7 +100,7 @@ class DecodeBatch:
             self.caches.append(kv)
         self.ws_ippd_bytes = L.ippd_decode_workspace_bytes(self.batches[0])
         self.ws_std_bytes = L.standard_decode_workspace_bytes(self.batches[0])
-        # zero-filled once: the library keeps its arrival counters at zero between calls
+        # the library needs no initialisation of its workspace (zeros for tidiness)
         self.ws_ippd = torch.zeros(max(self.ws_ippd_bytes, 256), dtype=torch.uint8, device=dev)
         self.ws_std = torch.zeros(max(self.ws_std_bytes, 256), dtype=torch.uint8, device=dev)
         self.q_rot = torch.empty(nt, hq, head_dim, dtype=td, device=dev)

@@ -92,13 +92,6 @@ def oracle_steps(st: W.Structure, kv: W.LayerKV, steps: Iterable[int], record: S
     return res
 
 
-def bookkeeping_zero(db: DecodeBatch) -> bool:
-    """The per-question merge bookkeeping at the head of both workspaces (Nt
-    uint32) is back at zero after every call."""
-    torch.cuda.synchronize()
-    return bool(torch.all(db.ws_ippd[: 4 * db.Nt] == 0)) and bool(torch.all(db.ws_std[: 4 * db.Nt] == 0))
-
-
 def max_err(gpu: np.ndarray, ref: np.ndarray) -> float:
     mask = ~np.isnan(ref)
     if not mask.any():

@@ -125,12 +125,12 @@ def test_workspace_validation(lib):
 
 
 def test_workspace_formula(lib):
-    # one counter per question, then (max_chunks + 1) * Nt * Hq partial states of
-    # D + 2 floats; each piece 256-byte rounded.  Both modes alike.
+    # (max_chunks + 1) * Nt * Hq partial states of D + 2 floats (chunks, then
+    # the segment), each array 256-byte rounded.  Both modes alike.
     bt = valid_batch(chunk_tokens=64)
     slots = (256 // 64 + 1) * 4 * 4
     r = lambda x: (x + 255) // 256 * 256
-    want = r(4 * 4) + r(slots * 64 * 4) + r(slots * 2 * 4)
+    want = r(slots * 64 * 4) + r(slots * 2 * 4)
     assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == want
     assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == want
 
