@@ -61,6 +61,9 @@ template <> struct Mfma<uint16_t> {   // bf16: one v_mfma_f32_16x16x32_bf16 per 
     return __builtin_bit_cast(Frag, *reinterpret_cast<const u32x4_t*>(a));
   }
   static __device__ __forceinline__ Frag zero() { return __builtin_bit_cast(Frag, u32x4_t{0u, 0u, 0u, 0u}); }
+  static __device__ __forceinline__ Frag ones() {   // bf16 1.0 = 0x3f80
+    return __builtin_bit_cast(Frag, u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+  }
   static __device__ __forceinline__ Frag keep_first(Frag f, int n) {
     u16x8_t u = __builtin_bit_cast(u16x8_t, f);
 #pragma unroll
@@ -93,6 +96,7 @@ template <> struct Mfma<float> {      // fp32: eight v_mfma_f32_16x16x4_f32 per 
     return Frag{x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
   }
   static __device__ __forceinline__ Frag zero() { return Frag{0, 0, 0, 0, 0, 0, 0, 0}; }
+  static __device__ __forceinline__ Frag ones() { return Frag{1, 1, 1, 1, 1, 1, 1, 1}; }
   static __device__ __forceinline__ Frag keep_first(Frag f, int n) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) f[e] = e < n ? f[e] : 0.f;
@@ -173,15 +177,58 @@ __device__ __forceinline__ void wait_tiles(int k) {
   }
 }
 
+// One 16-byte LDS-DMA from a wave-uniform base plus this lane's 32-bit
+// offset (the SGPR-base form: no per-lane 64-bit address arithmetic).
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds_block) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(sbase), "{m0}"(__builtin_amdgcn_readfirstlane(lds_block)) : "memory");
+}
+
+// This lane's byte offsets, from the tile's first token, of the 16 bytes it
+// fetches for each of its DMA blocks (blocks wave, wave + NW, ...) of a full
+// 32-token tile: K rows in MFMA order with swizzled 16-byte chunks, then the
+// values' four 8-token column blocks.  Keys and values of a tile both start
+// at element t0 * D of their arrays (t0 is a multiple of 8).
+template <typename T, int D, int NW, int NS>
+struct TileOffsets {
+  using R = Ring<T, D, NS>;
+  static constexpr int DPT = R::BLOCKS / NW;
+  uint32_t off[DPT];
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int d = 0; d < DPT; ++d) {
+      const int q = wave + NW * d;
+      if (q < R::KBLOCKS) {
+        const int r = q * (64 / R::CPR) + lane / R::CPR;
+        const int c = (lane % R::CPR) ^ ((r >> R::KSH) & R::KMASK);
+        off[d] = static_cast<uint32_t>(tile_token(r >> 4, r & 15) * D * R::E + c * 16);
+      } else {
+        off[d] = static_cast<uint32_t>((q - R::KBLOCKS) * 1024 + lane * 16);
+      }
+    }
+  }
+};
+
 // Issue the DMA blocks of one tile (tokens [t0, t0+32) of [.., k1)) owned by
-// this wave: blocks wave, wave + NW, ...  Tokens past k1 are clamped to the
-// last valid one; the compute masks them.
+// this wave: blocks wave, wave + NW, ...  A full tile uses the precomputed
+// offsets; in a partial one, tokens past k1 are clamped to the last valid
+// one (the compute masks them).
 template <typename T, int D, int NW, int NS>
 __device__ __forceinline__ void issue_tile(uint32_t stage, const T* __restrict__ kbase,
                                            const T* __restrict__ vbase, int64_t t0, int64_t k1, int wave,
-                                           int lane) {
+                                           int lane, const TileOffsets<T, D, NW, NS>& to) {
   using R = Ring<T, D, NS>;
   constexpr int DPT = R::BLOCKS / NW;
+  if (t0 + 32 <= k1) {
+    const T* kt = kbase + t0 * D;
+    const T* vt = vbase + t0 * D;
+#pragma unroll
+    for (int d = 0; d < DPT; ++d) {
+      const int q = wave + NW * d;          // wave-uniform
+      dma16s(q < R::KBLOCKS ? kt : vt, to.off[d], stage + static_cast<uint32_t>(q) * 1024u);
+    }
+    return;
+  }
   const int64_t vblk_last = (k1 - 1) >> 3;
 #pragma unroll
   for (int d = 0; d < DPT; ++d) {
@@ -206,39 +253,45 @@ __device__ __forceinline__ void issue_tile(uint32_t stage, const T* __restrict__
 
 // ---------------------------------------------------------------------------
 // Online softmax state of one 16-row block (O^T registers: lane (lg, lr)
-// holds row lr, dims 16*db + 4*lg + v).
+// holds row lr, dims 16*db + 4*lg + v).  The row sums come from the MFMA
+// unit: ls += ONES * P^T, an all-ones 16 x 32 V^T block, so every element of
+// ls is row lr's sum of the (rounded) weights, the same weights the values
+// are multiplied by.
 // ---------------------------------------------------------------------------
 template <int D>
 struct RowState {
   f32x4_t o[D / 16];
-  float m, l;
+  f32x4_t ls;
+  float m;
 };
 
 template <int D>
 __device__ __forceinline__ void row_init(RowState<D>& st) {
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) st.o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  st.ls = f32x4_t{0.f, 0.f, 0.f, 0.f};
   st.m = -INFINITY;
-  st.l = 0.f;
 }
 
 // Fold one tile's scores (lane (lg, lr): tokens 8*lg + 4*kb + v of row lr)
 // into the state; returns P^T as the B operand of the PV product.  The
-// running max m used as the exponent offset is raised only when some row's
+// running max m used as the exponent offset is raised only when some lane's
 // tile max exceeds it by more than kRescaleLog2 (in log2 units): below that
 // the weights exp2(c*(s - m)) stay under 2^kRescaleLog2, harmless in fp32,
-// and the rescale of the sum and the values is skipped.  Any offset at or
-// below the true max gives the same normalised result.
+// and the rescale of the sums and values is skipped.  Only that rare path
+// reduces the max across the four lanes of a row, so that the row's lanes
+// keep one common offset.  Any offset at or below the true max gives the
+// same normalised result.
 template <typename T, int D>
 __device__ __forceinline__ typename Mfma<T>::Frag softmax_step(const f32x4_t (&sc)[2], RowState<D>& st, float c) {
-  float mx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
-                   fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
-  mx = xor16_max(mx);
-  mx = xor32_max(mx);
-  if (__any((mx - st.m) * c > kRescaleLog2)) {
+  const float lmx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                          fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+  if (__any((lmx - st.m) * c > kRescaleLog2)) {
+    float mx = xor16_max(lmx);
+    mx = xor32_max(mx);
     const float mn = fmaxf(st.m, mx);
     const float alpha = fast_exp2((st.m - (mn == -INFINITY ? 0.f : mn)) * c);
-    st.l *= alpha;
+    st.ls *= alpha;
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) st.o[db] *= alpha;
     st.m = mn;
@@ -249,7 +302,6 @@ __device__ __forceinline__ typename Mfma<T>::Frag softmax_step(const f32x4_t (&s
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int v = 0; v < 4; ++v) pv[4 * kb + v] = fast_exp2(fmaf(sc[kb][v], c, -cm));
-  st.l += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
   return Mfma<T>::from_f32(pv);
 }
 
@@ -297,6 +349,8 @@ __device__ __forceinline__ void ring_tile(const unsigned char* stage, const type
   }
   const int keep = min(max(n - 8 * lg, 0), 8);
 #pragma unroll
+  for (int rb = 0; rb < RB; ++rb) st[rb].ls = M::mma(M::ones(), pf[rb], st[rb].ls);
+#pragma unroll
   for (int db = 0; db < D / 16; ++db) {
     // block lg holds this lane's 8 tokens; dimension 16*db + lr of it
     const unsigned char* vp = stage + R::KBYTES + lg * R::VBLK + (16 * db + lr) * 8 * R::E;
@@ -307,13 +361,129 @@ __device__ __forceinline__ void ring_tile(const unsigned char* stage, const type
   }
 }
 
+// The two halves of ring_tile, for the software-pipelined loop: qk_tile
+// computes the raw scores of a stage, softmax_pv folds them (n valid
+// tokens) into the row states and adds P^T times the stage's values.
+template <typename T, int D, int NS, int RB>
+__device__ __forceinline__ void qk_tile(const unsigned char* stage, const typename Mfma<T>::Frag (&qf)[RB][D / 32],
+                                        f32x4_t (&sc)[RB][2], int lr, int lg) {
+  using R = Ring<T, D, NS>;
+  using M = Mfma<T>;
+  constexpr int DS = D / 32;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int r = 16 * kb + lr;
+    const int sw = (r >> R::KSH) & R::KMASK;
+    const unsigned char* row = stage + r * (R::CPR * 16);
+    f32x4_t acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const int c0 = (8 * lg + 32 * ds) * R::E / 16;
+      const typename M::Frag kf = M::lds2(row + ((c0 ^ sw) * 16), row + (((c0 + 1) ^ sw) * 16));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb] = M::mma(kf, qf[rb][ds], acc[rb]);
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) sc[rb][kb] = acc[rb];
+  }
+}
+
+template <typename T, int D, int NS, int RB>
+__device__ __forceinline__ void softmax_pv(const unsigned char* stage, f32x4_t (&sc)[RB][2], RowState<D> (&st)[RB],
+                                           int n, int lr, int lg, float c) {
+  using R = Ring<T, D, NS>;
+  using M = Mfma<T>;
+  typename M::Frag pf[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (n < 32) mask_scores(sc[rb], n, lg);
+    pf[rb] = softmax_step<T, D>(sc[rb], st[rb], c);
+  }
+  const int keep = min(max(n - 8 * lg, 0), 8);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) st[rb].ls = M::mma(M::ones(), pf[rb], st[rb].ls);
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    const unsigned char* vp = stage + R::KBYTES + lg * R::VBLK + (16 * db + lr) * 8 * R::E;
+    typename M::Frag vf = M::lds2(vp, vp + 16);
+    if (n < 32) vf = M::keep_first(vf, keep);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st[rb].o[db] = M::mma(vf, pf[rb], st[rb].o[db]);
+  }
+}
+
+// One iteration of the software-pipelined loop: fold tile t (scores sc,
+// values at stv) and compute the scores of the next tile (keys at stk) into
+// sn.  The key reads go out first and are covered by the softmax VALU work;
+// the value reads go out behind the score MFMAs, which cover them; key and
+// value fragments are never live together.  On the last iteration stk is
+// any ring stage and sn is not used.
+template <typename T, int D, int NS, int RB>
+__device__ __forceinline__ void pipe_step(const unsigned char* stk, const unsigned char* stv,
+                                          const typename Mfma<T>::Frag (&qf)[RB][D / 32], f32x4_t (&sc)[RB][2],
+                                          f32x4_t (&sn)[RB][2], RowState<D> (&st)[RB], int n, int lr, int lg,
+                                          float c) {
+  using R = Ring<T, D, NS>;
+  using M = Mfma<T>;
+  constexpr int DS = D / 32, DB = D / 16;
+  typename M::Frag kf[2][DS], vf[DB];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int r = 16 * kb + lr;
+    const int sw = (r >> R::KSH) & R::KMASK;
+    const unsigned char* row = stk + r * (R::CPR * 16);
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      const int c0 = (8 * lg + 32 * ds) * R::E / 16;
+      kf[kb][ds] = M::lds2(row + ((c0 ^ sw) * 16), row + (((c0 + 1) ^ sw) * 16));
+    }
+  }
+  if (n < 32) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) mask_scores(sc[rb], n, lg);
+  }
+  typename M::Frag pf[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) pf[rb] = softmax_step<T, D>(sc[rb], st[rb], c);
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    f32x4_t acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb] = M::mma(kf[kb][ds], qf[rb][ds], acc[rb]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) sn[rb][kb] = acc[rb];
+  }
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const unsigned char* vp = stv + R::KBYTES + lg * R::VBLK + (16 * db + lr) * 8 * R::E;
+    vf[db] = M::lds2(vp, vp + 16);
+  }
+  if (n < 32) {
+    const int keep = min(max(n - 8 * lg, 0), 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) vf[db] = M::keep_first(vf[db], keep);   // never NaN * 0 past the end
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) st[rb].ls = M::mma(M::ones(), pf[rb], st[rb].ls);
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) st[rb].o[db] = M::mma(vf[db], pf[rb], st[rb].o[db]);
+}
+
 // Write one 16-row block's partial state to its slots.
 template <int D>
 __device__ __forceinline__ void publish_rows(const StepParams& p, const RowState<D>& st, int64_t slot, int lg) {
   float* dst = p.part_acc + slot * D + 4 * lg;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) *reinterpret_cast<f32x4_t*>(dst + 16 * db) = st.o[db];
-  if (lg == 0) *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(st.m, st.l);
+  if (lg == 0) *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(st.m, st.ls[0]);
 }
 
 __device__ __forceinline__ bool prompt_layout_ok(const StepParams& p, int b) {
@@ -597,6 +767,8 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   }
   RL rl;
   issue_row_loads<T, D, FUSED, RB>(rl, p, qi, h, lg);
+  TileOffsets<T, D, NW, NS> toff;
+  toff.init(wave, lane);
   // exactly P0 tiles go out before the one wait for the row loads (a unit
   // with fewer tiles fetches its last tile again): a single wait with a
   // fixed count leaves the compiler no reason to copy the loaded registers
@@ -604,7 +776,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   // ring's waits below stay sufficient.
 #pragma unroll
   for (int t = 0; t < P0; ++t)
-    issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane);
+    issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * min(t, ntiles - 1), k1, wave, lane, toff);
   wait_row_loads<(P0 * DPT < 63 ? P0 * DPT : 63)>(rl);
 
   bool act[RB];
@@ -625,7 +797,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   const bool live = __any(any_act);                // wave-uniform
 #pragma unroll
   for (int t = P0; t < RG::NS - 1; ++t)
-    if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane);
+    if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane, toff);
   RowState<D> st[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) row_init(st[rb]);
@@ -635,22 +807,51 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   // is refilled with tile t + NS - 1
   const int last = ntiles - 1;
   const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
-  for (int t = 0; t < ntiles; ++t) {
-    // tile t's blocks are this thread's oldest outstanding DMAs; those of
-    // tiles t+1 .. min(t+NS-2, last) are younger
-    wait_tiles<DPT, RG::NS - 2>(min(last - t, RG::NS - 2));
+  if constexpr (RG::NS >= 4) {
+    // software pipelined: iteration t folds tile t (softmax on the VALU, then
+    // P^T V on the MFMA) while the scores of tile t+1 are computed, so each
+    // wave has independent MFMA and VALU work in flight.  K of tile t+1 and
+    // V of tile t are both in the ring during iteration t.
+    f32x4_t sc[RB][2], sn[RB][2];
+    // tile 0's blocks are this thread's oldest DMAs; tiles 1 .. min(NS-2, last) are younger
+    wait_tiles<DPT, RG::NS - 2>(min(last, RG::NS - 2));
     __syncthreads();
-    const int tn = t + RG::NS - 1;
-    if (tn <= last)
-      issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane);
-    if (live) ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+    if (live) qk_tile<T, D, NS, RB>(ring, qf, sc, lr, lg);
+    for (int t = 0; t < ntiles; ++t) {
+      if (t < last) {
+        // tile t+1 must have landed; tiles t+2 .. min(t+NS-2, last) are younger
+        wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
+        __syncthreads();                            // also: every wave is past iteration t-1
+        const int tn = t + RG::NS - 1;
+        if (tn <= last)
+          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
+      }
+      if (live) {
+        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sc, sn,
+                                st, t == last ? tail_n : 32, lr, lg, c);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          sc[rb][0] = sn[rb][0];
+          sc[rb][1] = sn[rb][1];
+        }
+      }
+    }
+  } else {
+    for (int t = 0; t < ntiles; ++t) {
+      // tile t's blocks are this thread's oldest outstanding DMAs; those of
+      // tiles t+1 .. min(t+NS-2, last) are younger
+      wait_tiles<DPT, RG::NS - 2>(min(last - t, RG::NS - 2));
+      __syncthreads();
+      const int tn = t + RG::NS - 1;
+      if (tn <= last)
+        issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
+      if (live) ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
+    }
   }
   wait_vmcnt<0>();                                  // no LDS-DMA may outlive the workgroup
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    float l = xor16_sum(st[rb].l);
-    st[rb].l = xor32_sum(l);
     if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(chunk) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
   }
 }
@@ -845,20 +1046,19 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
     if (n < 32) mask_scores(sc, n, lg);
     const Frag pf = softmax_step<T, D>(sc, st, c);
     const int keep = min(max(n - 8 * lg, 0), 8);
+    st.ls = M::mma(M::ones(), pf, st.ls);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
       const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
       st.o[db] = M::mma(v, pf, st.o[db]);
     }
   }
-  float l = xor16_sum(st.l);
-  st.l = xor32_sum(l);
   __syncthreads();                                 // the query rows are dead
   if (live && ww < sw && lr < G) {
     float* o = reinterpret_cast<float*>(sh.main) + ((k * sw + ww) * G + lr) * (D + 4) + 4 * lg;
 #pragma unroll
     for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4_t*>(o + 16 * db) = st.o[db];
-    if (lg == 0) sh.ml[k * sw + ww][lr] = make_float2(st.m, st.l);
+    if (lg == 0) sh.ml[k * sw + ww][lr] = make_float2(st.m, st.ls[0]);
   }
   __syncthreads();
   // combine each task's wave states and its last key: item (task, row r, dims d0..d0+7)
@@ -1058,8 +1258,9 @@ static hipError_t launch_waves(int waves, int rb, bool deep, int grid, const Ste
     case 2: return launch_depth<T, D, 2, 1>(deep, grid, p, s);
     case 4: return launch_depth<T, D, 4, 1>(deep, grid, p, s);
     default:
-      // the planner gives fp32 at D = 128 at most four waves
-      if constexpr (sizeof(T) == 4 && D == 128) return hipErrorInvalidValue;
+      // the planner gives fp32 at D = 128 at most four waves, and bf16 at
+      // D = 128 eight waves only with two row blocks each
+      if constexpr (D == 128) return hipErrorInvalidValue;
       else return launch_depth<T, D, 8, 1>(deep, grid, p, s);
   }
 }

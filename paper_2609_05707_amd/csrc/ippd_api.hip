@@ -101,13 +101,16 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   }
   const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
   const int64_t ctx_blocks = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
-  // segment tasks (question, kv head): about two units per compute unit, at
-  // most `waves` tasks per unit, and all tasks' wave states must fit the
-  // smallest LDS ring (32 KB)
+  // segment tasks (question, kv head): as few per unit as keeps the segment
+  // units within one round of resident workgroups (they run after the
+  // context units), at most `waves` per unit, and all tasks' wave states
+  // must fit the smallest LDS ring (32 KB)
+  const bool deep = ctx_blocks <= compute_units() || wg_per_cu == 1;
+  const int64_t slots = static_cast<int64_t>(compute_units()) * (deep ? 1 : 2);
   const int64_t seg_tasks = static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   const int64_t state_bytes = static_cast<int64_t>(G) * (bt->head_dim + 4) * 4;
   int tpu = 1;
-  while (tpu < waves && seg_tasks / (2 * tpu) >= 2 * compute_units() && 2 * tpu * state_bytes <= 32768) tpu *= 2;
+  while (tpu < waves && (seg_tasks + tpu - 1) / tpu > slots && 2 * tpu * state_bytes <= 32768) tpu *= 2;
   const int64_t seg_blocks = (seg_tasks + tpu - 1) / tpu;
   const int64_t grid = ctx_blocks + seg_blocks;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
@@ -122,7 +125,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->ctx_blocks = static_cast<int>(ctx_blocks);
   pl->seg_blocks = static_cast<int>(seg_blocks);
   pl->seg_tpu = tpu;
-  pl->deep = (ctx_blocks <= compute_units() || wg_per_cu == 1) ? 1 : 0;
+  pl->deep = deep ? 1 : 0;
   pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = 0;
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));

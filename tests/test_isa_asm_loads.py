@@ -136,7 +136,7 @@ def test_scanner_flags_a_planted_copy():
                     reason="hipcc not available")
 def test_no_early_reads_of_asm_loads(tmp_path):
     out = tmp_path / "decode_step.s"
-    flags = [f for f in B.HIPCC_FLAGS if f != "-fPIC"]
+    flags = [f for f in B.flags_for("decode_step.hip") if f != "-fPIC"]
     cmd = [B.hipcc(), *flags, "--cuda-device-only", "-S", os.path.join(B.CSRC, "decode_step.hip"), "-o", str(out)]
     res = subprocess.run(cmd, capture_output=True, text=True)
     assert res.returncode == 0, res.stderr[-2000:]
