@@ -18,6 +18,7 @@ import csv
 import hashlib
 import json
 import os
+import re
 from collections import defaultdict
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -39,7 +40,8 @@ def per_dispatch(path: str, counter: str):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            key = "attend" if "attend_kernel" in name and "true>" in name else \
+            fused = re.search(r"attend_kernel<[^>]*\btrue\b", name) is not None
+            key = "attend" if fused else \
                   "merge" if "merge_kernel" in name else \
                   "copy" if "copyBuffer" in name else name
             vals[key].append(float(r["Counter_Value"]))
