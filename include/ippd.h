@@ -229,6 +229,48 @@ ippd_status_t standard_decode_step(const ippd_batch_t *batch, const void *q_new,
                                    float *out, float *lse, void *workspace, size_t workspace_bytes,
                                    hipStream_t stream);
 
+/*
+ * Stacked-prompt prefill attention (Sec. 4.1: the prompt header, every token
+ * a query row under the mask M_fin; App. A.2 prefill dimensions).  The cache
+ * holds the rotated context keys (ippd_load_context) and each question's
+ * tokens as its segment (ippd_load_segments with init_len = the question
+ * lengths, so seg_len[i] = |x_i|).  For context token t of prompt b and
+ * query head h (kv head g):
+ *   out_ctx[ctx_off[b] + t][h] = softmax_k(scale q . K_k) V_k over the
+ *                                prompt's context keys 0..t   (causal);
+ * for token u < seg_len[i] of question i (prompt b):
+ *   out_seg[i][u][h] = the same over ALL context keys of prompt b and the
+ *                      question's own keys 0..u   (M_ctx, M_qtn, M_caus),
+ * with the queries rotated at t and at ctx_len[b] + u.
+ * q_ctx [ctx_pool_tokens][Hq][D] and q_seg [Nt][seg_capacity][Hq][D] are raw
+ * (pre-rotation) queries of the batch dtype; out_ctx and out_seg have the
+ * same layouts in float32 (16-byte aligned).  Rows outside every prompt's
+ * context and slots at or past seg_len[i] are neither read nor written.
+ * IPPD serves all question tokens of a prompt from one pass over its
+ * context and computes the context rows once.
+ * max_prompt_question_tokens: host bound on the sum of seg_len over the
+ * questions of any one prompt (it sizes the grid); a prompt above it sets
+ * IPPD_FLAG_BAD_LAYOUT and not all of its question rows are written.
+ * active[] is ignored (every question is prefilled).  No workspace; one
+ * kernel launch.
+ */
+ippd_status_t ippd_prefill_attention(const ippd_batch_t *batch, int32_t max_prompt_question_tokens,
+                                     const void *q_ctx, const void *q_seg, const ippd_kv_cache_t *kv,
+                                     float *out_ctx, float *out_seg, hipStream_t stream);
+
+/*
+ * Baseline: the same outputs computed as standard prompting does it (Sec. 3:
+ * each question is its own prompt [context; question]): every question
+ * streams its prompt's context and recomputes the context rows (all copies
+ * write the same values to out_ctx).  Same arguments and semantics as
+ * ippd_prefill_attention, the bound applying per question, except that the
+ * context rows of a prompt without questions are not written (no question's
+ * prompt contains them).
+ */
+ippd_status_t standard_prefill_attention(const ippd_batch_t *batch, int32_t max_prompt_question_tokens,
+                                         const void *q_ctx, const void *q_seg, const ippd_kv_cache_t *kv,
+                                         float *out_ctx, float *out_seg, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *ippd_status_string(ippd_status_t status);
 

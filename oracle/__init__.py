@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for IPPD decode-step attention.
+"""fp64 CPU oracle for IPPD decode-step and prefill attention.
 
 TEST INFRASTRUCTURE ONLY.  Only the test suite, the package smoke check and
 the CPU-baseline leg of the benchmark may import or call anything here.  The
@@ -21,3 +21,4 @@ from .ippd import (  # noqa: F401
     mask_predicates,
     decode_run,
 )
+from . import prefill  # noqa: F401,E402

@@ -32,6 +32,7 @@ EXPORTED = [
     "ippd_decode_workspace_bytes", "standard_decode_workspace_bytes",
     "ippd_decode_attention", "standard_decode_attention",
     "ippd_decode_step", "standard_decode_step",
+    "ippd_prefill_attention", "standard_prefill_attention",
     "ippd_status_string", "ippd_last_hip_error", "ippd_version",
 ]
 
@@ -103,6 +104,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         getattr(lib, name).argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache),
                                        c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
         getattr(lib, name).restype = st
+    for name in ("ippd_prefill_attention", "standard_prefill_attention"):
+        getattr(lib, name).argtypes = [P(IppdBatch), ctypes.c_int32, c_void_p, c_void_p, P(IppdKvCache), c_void_p,
+                                       c_void_p, c_void_p]
+        getattr(lib, name).restype = st
     lib.ippd_status_string.argtypes = [c_int]
     lib.ippd_status_string.restype = ctypes.c_char_p
     lib.ippd_last_hip_error.argtypes = []
@@ -170,6 +175,19 @@ def standard_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, worksp
            load_library().standard_decode_step(ctypes.byref(batch), q_new, k_new, v_new, q_rot,
                                                ctypes.byref(kv), out, lse, workspace, workspace_bytes,
                                                stream))
+
+
+def ippd_prefill_attention(batch, max_prompt_question_tokens, q_ctx, q_seg, kv, out_ctx, out_seg, stream) -> None:
+    _check("ippd_prefill_attention",
+           load_library().ippd_prefill_attention(ctypes.byref(batch), max_prompt_question_tokens, q_ctx, q_seg,
+                                                 ctypes.byref(kv), out_ctx, out_seg, stream))
+
+
+def standard_prefill_attention(batch, max_prompt_question_tokens, q_ctx, q_seg, kv, out_ctx, out_seg,
+                               stream) -> None:
+    _check("standard_prefill_attention",
+           load_library().standard_prefill_attention(ctypes.byref(batch), max_prompt_question_tokens, q_ctx, q_seg,
+                                                     ctypes.byref(kv), out_ctx, out_seg, stream))
 
 
 def raw_status(fn: str, *args) -> int:

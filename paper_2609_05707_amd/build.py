@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libippd.so")
 
-SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip"]
+SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip", "prefill.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -32,6 +32,7 @@ HIPCC_FLAGS = [
 # its MFMA/permlane inputs: without this every max costs two instructions.
 SOURCE_FLAGS = {
     "decode_step.hip": ["-fno-honor-nans"],
+    "prefill.hip": ["-fno-honor-nans"],
 }
 
 

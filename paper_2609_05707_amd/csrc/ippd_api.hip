@@ -196,6 +196,64 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));
 }
 
+
+// Launch plan of a prefill call (host fields only).
+bool plan_prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens, ippd::PrefillPlan* pl) {
+  if (check_batch(bt) != IPPD_OK || max_q_tokens < 0) return false;
+  int waves = 0, rb = 0;
+  if (!ippd::prefill_variant(bt->dtype, bt->head_dim, &waves, &rb)) return false;
+  const int G = bt->num_q_heads / bt->num_kv_heads;
+  const int tb = 16 * rb * waves / G;
+  const int64_t n_groups = static_cast<int64_t>(shared ? bt->num_prompts : bt->num_questions) * bt->num_kv_heads;
+  const int64_t gps = (n_groups + 7) / 8;
+  const int64_t qtok = shared ? max_q_tokens : (max_q_tokens < bt->seg_capacity ? max_q_tokens : bt->seg_capacity);
+  const int64_t kq = (qtok + tb - 1) / tb, kc = (static_cast<int64_t>(bt->max_ctx_len) + tb - 1) / tb;
+  const int64_t q_blocks = 8 * gps * kq, grid = q_blocks + 8 * gps * kc;
+  if (grid > (1ll << 30)) return false;
+  pl->shared = shared ? 1 : 0;
+  pl->waves = waves;
+  pl->rb = rb;
+  pl->tb = tb;
+  pl->n_groups = static_cast<int>(n_groups);
+  pl->gps = static_cast<int>(gps);
+  pl->kq = static_cast<int>(kq);
+  pl->kc = static_cast<int>(kc);
+  pl->q_blocks = static_cast<int>(q_blocks);
+  pl->grid = static_cast<int>(grid);
+  return true;
+}
+
+// Shared body of the two prefill entry points.
+ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens, const void* q_ctx,
+                      const void* q_seg, const ippd_kv_cache_t* kv, float* out_ctx, float* out_seg,
+                      hipStream_t stream) {
+  ippd_status_t st = check_batch(bt);
+  if (st != IPPD_OK) return st;
+  if (!q_ctx || !q_seg || !kv || !out_ctx || !out_seg || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt)
+    return IPPD_ERR_NULL;
+  if (!aligned16(q_ctx) || !aligned16(q_seg) || !aligned16(out_ctx) || !aligned16(out_seg) ||
+      !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) || !aligned16(kv->seg_vt))
+    return IPPD_ERR_ALIGN;
+  ippd::PrefillPlan pl;
+  if (!plan_prefill(bt, shared, max_q_tokens, &pl)) return IPPD_ERR_SHAPE;
+  if (pl.grid == 0) return IPPD_OK;
+  ippd::PrefillParams p;
+  p.q_ctx = q_ctx; p.q_seg = q_seg;
+  p.ctx_k = kv->ctx_k; p.ctx_vt = kv->ctx_vt; p.seg_k = kv->seg_k; p.seg_vt = kv->seg_vt;
+  p.ctx_off = bt->ctx_off; p.ctx_len = bt->ctx_len; p.q_start = bt->q_start; p.seg_len = bt->seg_len;
+  p.err_flag = bt->err_flag;
+  p.out_ctx = out_ctx; p.out_seg = out_seg;
+  p.pool = bt->ctx_pool_tokens;
+  p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hq = bt->num_q_heads; p.Hkv = bt->num_kv_heads;
+  p.G = bt->num_q_heads / bt->num_kv_heads; p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
+  p.max_ctx_len = bt->max_ctx_len;
+  p.shared = pl.shared; p.tb = pl.tb; p.n_groups = pl.n_groups; p.gps = pl.gps;
+  p.kq = pl.kq; p.kc = pl.kc; p.q_blocks = pl.q_blocks;
+  p.c = softmax_scale(bt) * 1.4426950408889634f;
+  fill_inv_freq(bt, p.inv_freq);
+  return hip_status(ippd::launch_prefill(bt->dtype, bt->head_dim, pl.grid, p, stream));
+}
+
 }  // namespace
 
 extern "C" {
@@ -293,6 +351,18 @@ ippd_status_t standard_decode_step(const ippd_batch_t* bt, const void* q_new, co
                 workspace_bytes, stream);
 }
 
+ippd_status_t ippd_prefill_attention(const ippd_batch_t* bt, int32_t max_prompt_question_tokens,
+                                     const void* q_ctx, const void* q_seg, const ippd_kv_cache_t* kv,
+                                     float* out_ctx, float* out_seg, hipStream_t stream) {
+  return prefill(bt, true, max_prompt_question_tokens, q_ctx, q_seg, kv, out_ctx, out_seg, stream);
+}
+
+ippd_status_t standard_prefill_attention(const ippd_batch_t* bt, int32_t max_prompt_question_tokens,
+                                         const void* q_ctx, const void* q_seg, const ippd_kv_cache_t* kv,
+                                         float* out_ctx, float* out_seg, hipStream_t stream) {
+  return prefill(bt, false, max_prompt_question_tokens, q_ctx, q_seg, kv, out_ctx, out_seg, stream);
+}
+
 const char* ippd_status_string(ippd_status_t s) {
   switch (s) {
     case IPPD_OK: return "ok";
@@ -308,6 +378,6 @@ const char* ippd_status_string(ippd_status_t s) {
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 400; }
+int ippd_version(void) { return 500; }
 
 }  // extern "C"

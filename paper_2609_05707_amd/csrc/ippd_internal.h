@@ -59,6 +59,35 @@ struct StepPlan {
   size_t workspace_bytes;
 };
 
+// Launch plan of one prefill call.  A group is (prompt b, kv head g) for
+// IPPD or (question i, kv head g) for the standard baseline.  A unit serves
+// tb query tokens x G heads (16 * rb * waves rows): question-row units (the
+// group's question tokens against its whole context and their own
+// questions) come first, then context-row units (causal over the context),
+// the longest causal blocks first.  Unit u of either kind runs on XCD u & 7,
+// which holds every unit of groups g = 8 j + (u & 7).
+struct PrefillPlan {
+  int shared, waves, rb, tb;
+  int n_groups, gps;       // groups, and groups per XCD slice (ceil(n_groups / 8))
+  int kq, kc;              // question-row and context-row units per group
+  int q_blocks, grid;      // 8 * gps * kq, then + 8 * gps * kc
+};
+
+struct PrefillParams {
+  const void* q_ctx;       // [pool][Hq][D] raw queries of context tokens
+  const void* q_seg;       // [Nt][seg_cap][Hq][D] raw queries of question tokens
+  const void* ctx_k; const void* ctx_vt; const void* seg_k; const void* seg_vt;
+  const int64_t* ctx_off; const int32_t* ctx_len; const int32_t* q_start; const int32_t* seg_len;
+  int32_t* err_flag;
+  float* out_ctx;          // [pool][Hq][D]
+  float* out_seg;          // [Nt][seg_cap][Hq][D]
+  int64_t pool;
+  int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len;
+  int shared, tb, n_groups, gps, kq, kc, q_blocks;
+  float c;                 // scale * log2(e)
+  double inv_freq[kMaxHalfDim];
+};
+
 struct StepParams {
   const void* q_new; const void* k_new; const void* v_new;   // fused step: raw token inputs
   const void* q_rot_in;                                        // attention only: rotated queries
@@ -83,5 +112,10 @@ hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
 hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s);
+// prefill_kernel for the batch dtype and head dimension (waves / rb fixed per
+// variant: see prefill_variant)
+hipError_t launch_prefill(int dtype, int head_dim, int grid, const PrefillParams& p, hipStream_t s);
+// (waves, rb) of the prefill variant for a dtype and head dimension; false if none
+bool prefill_variant(int dtype, int head_dim, int* waves, int* rb);
 
 }  // namespace ippd

@@ -207,3 +207,39 @@ class DecodeBatch:
         ws, wsb = (self.ws_std, self.ws_std_bytes) if standard else (self.ws_ippd, self.ws_ippd_bytes)
         fn(self.batches[layer], q_new.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), qr, self.caches[layer],
            out.data_ptr(), lse_ptr, ws.data_ptr(), wsb, self.stream())
+
+    # ------------------------------------------------------------------ prefill
+    def pack_prefill_queries(self, ctx_q, seg_q, seg_len0):
+        """Raw prefill queries in the library layouts: q_ctx [pool][Hq][D] (prompt
+        b's context token t at row ctx_off[b] + t) and q_seg [Nt][seg_capacity][Hq][D]
+        (question i's token u at [i][u]).  ctx_q [sum Lc, Hq, D] and seg_q
+        [sum seg_len0, Hq, D] are packed in prompt / question order."""
+        cq, sq = self.to_dev(ctx_q), self.to_dev(seg_q)
+        q_ctx = torch.zeros(self.pool, self.hq, self.D, dtype=self.tdtype, device=self.device)
+        src = 0
+        for b in range(self.B):
+            n, o = int(self.ctx_len[b]), int(self.ctx_off[b])
+            q_ctx[o:o + n] = cq[src:src + n]
+            src += n
+        nt = max(self.Nt, 1)
+        q_seg = torch.zeros(nt, self.seg_cap, self.hq, self.D, dtype=self.tdtype, device=self.device)
+        starts = np.concatenate([[0], np.cumsum(np.asarray(seg_len0, dtype=np.int64))])
+        for i in range(self.Nt):
+            n = int(starts[i + 1] - starts[i])
+            q_seg[i, :n] = sq[starts[i]:starts[i] + n]
+        return q_ctx, q_seg
+
+    def prefill_outputs(self, fill: float = 0.0):
+        """float32 out_ctx [pool][Hq][D] and out_seg [Nt][seg_capacity][Hq][D]."""
+        nt = max(self.Nt, 1)
+        oc = torch.full((self.pool, self.hq, self.D), fill, dtype=torch.float32, device=self.device)
+        os_ = torch.full((nt, self.seg_cap, self.hq, self.D), fill, dtype=torch.float32, device=self.device)
+        return oc, os_
+
+    def prefill(self, layer: int, q_ctx: torch.Tensor, q_seg: torch.Tensor, out_ctx: torch.Tensor,
+                out_seg: torch.Tensor, max_prompt_question_tokens: int, standard: bool = False) -> None:
+        """Prefill attention of every context and question token (the segments hold
+        the question tokens: load them with load_segments first)."""
+        fn = L.standard_prefill_attention if standard else L.ippd_prefill_attention
+        fn(self.batches[layer], int(max_prompt_question_tokens), q_ctx.data_ptr(), q_seg.data_ptr(),
+           self.caches[layer], out_ctx.data_ptr(), out_seg.data_ptr(), self.stream())

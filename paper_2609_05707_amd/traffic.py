@@ -26,7 +26,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("decode_step.hip", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
+    for f in ("decode_step.hip", "tile_attend.h", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
         with open(os.path.join(ROOT, "paper_2609_05707_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -94,6 +94,9 @@ def test_batch_validation(lib, field, value, status):
     assert decode_status(lib, bt) == status
     assert lib.ippd_append_kv(ctypes.byref(bt), FAKE, FAKE, FAKE, FAKE, ctypes.byref(kv_cache()), None) == status
     assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == 0
+    for fn in ("ippd_prefill_attention", "standard_prefill_attention"):
+        assert getattr(lib, fn)(ctypes.byref(bt), 8, FAKE, FAKE, ctypes.byref(kv_cache()), FAKE, FAKE,
+                                None) == status
 
 
 def test_pointer_validation(lib):
@@ -147,3 +150,22 @@ def test_step_pointer_validation(lib):
 def test_no_questions_is_a_noop(lib):
     bt = valid_batch(num_questions=0)
     assert decode_status(lib, bt, ws=None, ws_bytes=0) == L.IPPD_OK
+
+
+def test_prefill_validation(lib):
+    bt = valid_batch()
+    for fn in ("ippd_prefill_attention", "standard_prefill_attention"):
+        f = getattr(lib, fn)
+
+        def call(m=64, qc=FAKE, qs=FAKE, oc=FAKE, os_=FAKE, kv=None):
+            return f(ctypes.byref(bt), m, qc, qs, ctypes.byref(kv or kv_cache()), oc, os_, None)
+        assert call(qc=None) == L.IPPD_ERR_NULL
+        assert call(qs=None) == L.IPPD_ERR_NULL
+        assert call(oc=None) == L.IPPD_ERR_NULL
+        assert call(os_=None) == L.IPPD_ERR_NULL
+        assert call(kv=kv_cache(0)) == L.IPPD_ERR_NULL
+        assert call(qs=MISALIGNED) == L.IPPD_ERR_ALIGN
+        assert call(oc=MISALIGNED) == L.IPPD_ERR_ALIGN
+        assert call(kv=kv_cache(MISALIGNED)) == L.IPPD_ERR_ALIGN
+        assert call(m=-1) == L.IPPD_ERR_SHAPE
+    assert lib.ippd_version() >= 500

@@ -16,7 +16,9 @@ still-decoding questions (Sec. 4.4).  The synthetic recipe, per workload:
   (question tokens + already-fed answer tokens), stop step per question;
 * layer stream ``default_rng([wid, 1, layer])``: raw context K, context V,
   raw segment K, segment V, in that order, ``standard_normal * value_std``;
-* step stream ``default_rng([wid, 2, layer, step])``: q_new, k_new, v_new.
+* step stream ``default_rng([wid, 2, layer, step])``: q_new, k_new, v_new;
+* prefill stream ``default_rng([wid, 3, layer])``: raw queries of every
+  context token, then of every segment token (the rows of a prefill).
 
 Values are drawn as float32; bf16 workloads are then rounded to the nearest
 bf16 value (ties to even) and kept as float32 arrays holding bf16 values.
@@ -37,6 +39,7 @@ __all__ = [
     "make_structure",
     "layer_kv",
     "step_inputs",
+    "prefill_queries",
     "round_to_bf16",
     "bf16_bits",
 ]
@@ -217,3 +220,18 @@ def custom_workload(**kw) -> DecodeWorkload:
                 steps=1)
     base.update(kw)
     return DecodeWorkload(**base)
+
+
+@dataclass
+class PrefillQueries:
+    ctx_q: np.ndarray   # [sum Lc, Hq, D]        raw queries of the context tokens
+    seg_q: np.ndarray   # [sum seg_len0, Hq, D]  raw queries of the segment tokens
+
+
+def prefill_queries(st: Structure, layer: int = 0) -> PrefillQueries:
+    """Raw query vectors of every token of the stacked header (prefill rows)."""
+    wl = st.wl
+    rng = np.random.default_rng([wl.wid, 3, layer])
+    cq = _draw(rng, (int(st.ctx_start[-1]), wl.hq, wl.head_dim), wl)
+    sq = _draw(rng, (int(st.seg_start[-1]), wl.hq, wl.head_dim), wl)
+    return PrefillQueries(cq, sq)
