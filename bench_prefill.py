@@ -1,0 +1,179 @@
+#!/usr/bin/env python3
+"""Benchmark of the stacked-prompt prefill attention on one MI355X.
+
+For each workload, one prefill call computes the attention output of every
+header token (every context token and every question token of every
+prompt) for one layer; ippd_prefill_attention serves all question tokens of
+a prompt from one pass over its context and computes the context rows once,
+standard_prefill_attention prefills each question's own prompt
+[context; question] (Sec. 3, standard prompting).  Both run on identical
+caches and queries; the timed region is R calls back to back on one stream
+(HIP events on that stream), after W warmup calls.
+
+Reported per workload (one JSON line each):
+  value        header tokens per second of the IPPD call (sum of context and
+               question tokens / seconds per call);
+  roofline     bound "mfma": algorithmic FLOPs of one call (4*D per visible
+               (row, key) pair and query head: Q.K and P.V) / its time,
+               against the dense bf16 MFMA peak of 2500 TFLOP/s;
+  standard     the baseline's time, its FLOPs (the context rows recomputed
+               once per question) and the IPPD speedup;
+  cpu_baseline the fp64 oracle on a bounded sample of rows (host cores).
+
+Usage: python bench_prefill.py [--workload NAME|all] [--reps 20] [--warmup 3]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workload as W  # noqa: E402
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+WORKLOADS = {
+    # Llama-3-8B attention shape, one prompt: context 4096, 16 questions of 32 tokens.
+    "llama3-8b-lc4096-n16-q32": dict(wid=500, num_prompts=1, ctx_len=(4096, 4096), questions=(16, 16),
+                                     question_tokens=32, seg_len=(0, 0)),
+    # NarrativeQA-like shape (shared context ~3.5k tokens, ~30 questions of ~12 tokens).
+    "narrativeqa-shape-lc3500-n30-q12": dict(wid=501, num_prompts=1, ctx_len=(3500, 3500), questions=(30, 30),
+                                             question_tokens=12, seg_len=(0, 0)),
+    # 8 ragged prompts: context U{1024..8192}, 4..32 questions of U{8..32} tokens.
+    "ragged-b8": dict(wid=502, num_prompts=8, ctx_len=(1024, 8192), questions=(4, 32), question_tokens=0,
+                      seg_len=(8, 32)),
+}
+
+
+def make(name: str) -> W.DecodeWorkload:
+    return W.custom_workload(name=name, dtype="bf16", hq=32, hkv=8, head_dim=128, steps=1, value_std=0.5,
+                             **WORKLOADS[name])
+
+
+def flops(st: W.Structure, standard: bool) -> float:
+    """Algorithmic FLOPs of one call: 4*D*Hq per visible (query row, key) pair."""
+    wl = st.wl
+    per = 4.0 * wl.head_dim * wl.hq
+    tot = 0.0
+    for b in range(wl.num_prompts):
+        lc = int(st.ctx_len[b])
+        qs = range(int(st.q_start[b]), int(st.q_start[b + 1]))
+        ctx_pairs = lc * (lc + 1) / 2
+        tot += per * ctx_pairs * (len(qs) if standard else 1)   # context rows: once per question / once
+        for i in qs:
+            s = int(st.seg_len0[i])
+            tot += per * (s * lc + s * (s + 1) / 2)
+    return tot
+
+
+def cpu_baseline(st, kv, pq, budget_rows: int):
+    """The fp64 oracle on the first question rows and evenly spaced context rows."""
+    from oracle import prefill as P
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    nc = int(st.ctx_start[-1])
+    ctx_rows = np.linspace(0, nc - 1, num=budget_rows // 2).astype(int).tolist()
+    seg_rows = list(range(min(budget_rows // 2, int(st.seg_start[-1]))))
+    t0 = time.perf_counter()
+    P.prefill_standard(kv.ctx_k, kv.ctx_v, pq.ctx_q, st.ctx_start, st.q_start, kv.seg_k, kv.seg_v, pq.seg_q,
+                       st.seg_start, st.wl.rope_base, ctx_rows=ctx_rows, seg_rows=seg_rows)
+    dt = time.perf_counter() - t0
+    n = len(ctx_rows) + len(seg_rows)
+    return {"value": n / dt, "unit": "header tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(ctx_rows)} context rows (evenly spaced) + {len(seg_rows)} question rows, all heads, "
+                      f"{dt:.1f} s of fp64 numpy", "seconds": round(dt, 2)}
+
+
+def run(name: str, reps: int, warmup: int, cpu_rows: int):
+    import torch
+    from paper_2609_05707_amd.session import DecodeBatch
+
+    wl = make(name)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    pq = W.prefill_queries(st)
+    cap = max(8, int(st.seg_len0.max()))
+    db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
+                     rope_base=wl.rope_base)
+    db.load_context(0, kv.ctx_k, kv.ctx_v)
+    db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
+    q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0)
+    oc, os_ = db.prefill_outputs()
+    bound = max(int(st.seg_len0[st.q_start[b]:st.q_start[b + 1]].sum()) for b in range(wl.num_prompts))
+    stream = torch.cuda.current_stream()
+
+    def timed(standard):
+        for _ in range(warmup):
+            db.prefill(0, q_ctx, q_seg, oc, os_, bound, standard=standard)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            db.prefill(0, q_ctx, q_seg, oc, os_, bound, standard=standard)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3 / reps
+
+    t_ippd = timed(False)
+    t_std = timed(True)
+    assert db.err_flag() == 0
+    tokens = int(st.ctx_start[-1] + st.seg_start[-1])
+    f_ippd, f_std = flops(st, False), flops(st, True)
+    achieved = f_ippd / t_ippd / 1e12
+    res = {
+        "metric": "stacked-prompt prefill attention: header tokens/s, 1 MI355X",
+        "value": round(tokens / t_ippd, 1),
+        "unit": "header tokens/s",
+        "n_gpus": 1,
+        "reps": reps,
+        "warmup": warmup,
+        "ms_per_call": round(t_ippd * 1e3, 4),
+        "higher_is_better": True,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normal K/V/Q, rounded to bf16; no dataset)",
+        "config": {"workload": f"{name}: B={wl.num_prompts}, Hq={wl.hq}, Hkv={wl.hkv}, D={wl.head_dim}, "
+                               f"Lc={wl.ctx_len}, N={wl.questions}, question tokens "
+                               f"{wl.question_tokens or wl.seg_len}",
+                   "header_tokens": tokens, "layers": 1},
+        "roofline": {"bound": "mfma", "kernel": "prefill_kernel (one ippd_prefill_attention call)",
+                     "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "algorithmic_flops_per_call": f_ippd, "avg_call_us": round(t_ippd * 1e6, 2)},
+        "standard": {"ms_per_call": round(t_std * 1e3, 4), "algorithmic_flops_per_call": f_std,
+                     "achieved_tflops": round(f_std / t_std / 1e12, 1), "ippd_speedup": round(t_std / t_ippd, 3),
+                     "flop_ratio": round(f_std / f_ippd, 3)},
+    }
+    if cpu_rows > 0:
+        res["cpu_baseline"] = cpu_baseline(st, kv, pq, cpu_rows)
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--workload", default="all", choices=["all", *WORKLOADS])
+    ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-rows", type=int, default=64, help="rows the oracle computes (0 = skip)")
+    args = ap.parse_args()
+    import torch
+    assert torch.cuda.is_available(), "bench_prefill.py needs a GPU"
+    torch.cuda.set_device(0)
+    names = list(WORKLOADS) if args.workload == "all" else [args.workload]
+    for n in names:
+        print(json.dumps(run(n, args.reps, args.warmup, args.cpu_rows)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -30,7 +30,8 @@
 // Question-row units come first in the grid (each streams a whole context),
 // then context-row units, longest causal block first.  Unit u of either kind
 // runs on XCD u & 7, which holds every unit of the groups 8j + (u & 7): the
-// units of a group share its tiles through that XCD's L2.
+// units of a group share its tiles through that XCD's L2.  Groups are
+// numbered kv head minor, so each XCD gets its share of every prompt.
 #include <float.h>
 #include <stddef.h>
 
@@ -83,14 +84,16 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
   const int G = p.G, TB = p.tb;
 
   int b, g, qa, nq;
+  // kv head minor: the XCD slice (group % 8) cycles over kv heads, which
+  // carry equal work, rather than over prompts of different lengths
   if (p.shared) {
-    g = grp / p.B;
-    b = grp - g * p.B;
+    b = grp / p.Hkv;
+    g = grp - b * p.Hkv;
     qa = p.q_start[b];
     nq = p.q_start[b + 1] - qa;
   } else {
-    g = grp / p.Nt;
-    qa = grp - g * p.Nt;
+    qa = grp / p.Hkv;
+    g = grp - qa * p.Hkv;
     nq = 1;
     b = prompt_of(p.q_start, p.B, qa);
   }
