@@ -97,6 +97,22 @@ typedef struct ippd_batch {
   int32_t       *seg_len;    /* [Nt]  cached segment tokens; advanced by ippd_append_kv */
   const uint8_t *active;     /* [Nt]  1 = decoding this step */
   int32_t       *err_flag;   /* [1]   IPPD_FLAG_* bits (never cleared by the library) */
+  /* Two-level sharing (optional; Sec. 4.4: one stacked prompt holds several
+   * contexts behind one instruction p, which is then read once for all of
+   * their questions).  num_instr = S instruction blocks; prompts
+   * instr_start[s] .. instr_start[s+1]-1 sit behind instruction s
+   * (instr_start[0] = 0, instr_start[S] = B, non-decreasing).  Instruction s
+   * occupies pool tokens [instr_off[s], instr_off[s] + instr_len[s]) of the
+   * context pool (instr_off a multiple of 8) at positions 0..instr_len[s]-1;
+   * the contexts behind it and their questions move up by instr_len[s]
+   * (Sec. 4.1: p at [0, |p|), c_j from |p|).  num_instr = 0 disables the
+   * level and the fields below are not read. */
+  int32_t num_instr;            /* S >= 0 */
+  int32_t max_instr_len;        /* host bound on instr_len[s], <= ctx_pool_tokens */
+  int32_t max_instr_questions;  /* host bound on the questions behind one instruction, >= 1 */
+  const int32_t *instr_start;   /* [S+1] */
+  const int64_t *instr_off;     /* [S] */
+  const int32_t *instr_len;     /* [S] */
 } ippd_batch_t;
 
 /*
@@ -121,7 +137,8 @@ typedef struct ippd_kv_cache {
  * Fill the context part of the cache from raw (pre-rotation) keys and values
  * k_raw/v_raw [ctx_pool_tokens][Hkv][D], laid out like the pool: token t of
  * prompt b is row ctx_off[b] + t and is rotated at position t (Sec. 4.1:
- * context tokens sit at [|p|, |p| + |c_j|), with p folded into the context).
+ * context tokens sit at [|p|, |p| + |c_j|), with p folded into the context),
+ * or at instr_len[s] + t behind instruction s of a two-level batch.
  * Rows outside every prompt's range are neither read nor written.
  * Stands in for the prefill that would produce this cache.
  */
@@ -130,9 +147,22 @@ ippd_status_t ippd_load_context(const ippd_batch_t *batch, const void *k_raw,
                                 hipStream_t stream);
 
 /*
+ * Fill the instruction blocks of a two-level batch (num_instr > 0) from raw
+ * keys/values laid out like the pool, k_raw/v_raw [ctx_pool_tokens][Hkv][D]:
+ * token t of instruction s is row instr_off[s] + t and is rotated at
+ * position t (Sec. 4.1: p occupies [0, |p|)).  Other rows are neither read
+ * nor written, so one raw buffer may hold both the instructions and the
+ * contexts (call ippd_load_context for the latter).
+ */
+ippd_status_t ippd_load_instructions(const ippd_batch_t *batch, const void *k_raw,
+                                     const void *v_raw, const ippd_kv_cache_t *kv,
+                                     hipStream_t stream);
+
+/*
  * Fill segments from raw keys/values k_raw/v_raw [Nt][seg_capacity][Hkv][D]:
  * slots 0..init_len[i]-1 of question i are rotated at ctx_len[b] + slot
- * (Sec. 4.1 question/answer positions) and seg_len[i] is set to init_len[i]
+ * (plus instr_len[s] behind instruction s of a two-level batch; Sec. 4.1
+ * question/answer positions) and seg_len[i] is set to init_len[i]
  * (device [Nt], each <= seg_capacity; larger values set IPPD_FLAG_BAD_LAYOUT
  * and leave the question untouched).
  */
@@ -145,7 +175,7 @@ ippd_status_t ippd_load_segments(const ippd_batch_t *batch, const void *k_raw,
  * tokens; Sec. 4.2: each generated token re-enters the prompt at its virtual
  * position for the next step).
  * For every active question i of prompt b, with s = seg_len[i] and
- * pos = ctx_len[b] + s:
+ * pos = ctx_len[b] + s (plus instr_len of b's instruction in a two-level batch):
  *   q_rot[i][h] = R(pos) q_new[i][h]        for all Hq heads,
  *   seg slot s of (i, g) <- (R(pos) k_new[i][g], v_new[i][g]),
  *   seg_len[i] = s + 1.
@@ -177,10 +207,11 @@ size_t standard_decode_workspace_bytes(const ippd_batch_t *batch);
  *   out[i][h] = softmax_k( scale * q_rot[i][h] . K_k ) V_k
  * over the keys of prompt b's context and of segment (i, g) slots
  * 0..seg_len[i]-1 (call after ippd_append_kv, so the step's own token is the
- * last key).  Each context tile is read from HBM once for ALL active
- * questions and all heads of its kv group; the context is split into chunks
- * whose partial softmax states (max, sum, weighted values) are merged
- * exactly.  lse[i][h] = natural-log sum of exp over the same logits
+ * last key), and, in a two-level batch, of b's instruction.  Each context
+ * tile is read from HBM once for ALL active questions and all heads of its
+ * kv group, each instruction tile once for all questions of all prompts
+ * behind it; contexts and instructions are split into chunks whose partial
+ * softmax states (max, sum, weighted values) are merged exactly.  lse[i][h] = natural-log sum of exp over the same logits
  * (optional, may be NULL).  out [Nt][Hq][D] and lse [Nt][Hq] are float32;
  * rows of inactive questions are not written.
  * workspace: >= ippd_decode_workspace_bytes(batch) bytes (see above).
@@ -215,7 +246,9 @@ ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q
  * q_rot [Nt][Hq][D] receives the rotated queries, or may be NULL.  An active
  * question whose segment is full (seg_len[i] == seg_capacity) sets
  * IPPD_FLAG_SEGMENT_FULL and gets no output row.  workspace as for
- * ippd_decode_attention.
+ * ippd_decode_attention.  In a two-level batch the call runs
+ * ippd_append_kv and ippd_decode_attention as three launches (q_rot is then
+ * required).
  */
 ippd_status_t ippd_decode_step(const ippd_batch_t *batch, const void *q_new, const void *k_new,
                                const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,
@@ -252,7 +285,8 @@ ippd_status_t standard_decode_step(const ippd_batch_t *batch, const void *q_new,
  * questions of any one prompt (it sizes the grid); a prompt above it sets
  * IPPD_FLAG_BAD_LAYOUT and not all of its question rows are written.
  * active[] is ignored (every question is prefilled).  No workspace; one
- * kernel launch.
+ * kernel launch.  Two-level batches (num_instr > 0) are not supported here
+ * (IPPD_ERR_SHAPE).
  */
 ippd_status_t ippd_prefill_attention(const ippd_batch_t *batch, int32_t max_prompt_question_tokens,
                                      const void *q_ctx, const void *q_seg, const ippd_kv_cache_t *kv,

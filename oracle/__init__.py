@@ -15,6 +15,7 @@ from .ippd import (  # noqa: F401
     attend,
     standard_prompting_question,
     KVState,
+    Instructions,
     decode_step_standard,
     stacked_prompt_step,
     build_stacked_metadata,

@@ -140,14 +140,35 @@ class KVState:
             self.seg_v[i] = np.concatenate([self.seg_v[i], v_new[i][None]], axis=0)
 
 
+@dataclass
+class Instructions:
+    """Instruction blocks of a two-level batch (Sec. 4.4: one stacked prompt
+    holds several contexts behind one instruction p): prompts
+    prompt_start[s]:prompt_start[s+1] sit behind instruction s, whose raw
+    keys/values are k/v[tok_start[s]:tok_start[s+1]]."""
+
+    prompt_start: np.ndarray
+    tok_start: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+
+    def of_prompt(self, b: int):
+        s = int(np.searchsorted(self.prompt_start, b, side="right") - 1)
+        t0, t1 = int(self.tok_start[s]), int(self.tok_start[s + 1])
+        return self.k[t0:t1], self.v[t0:t1]
+
+
 def decode_step_standard(ctx_k, ctx_v, ctx_start, q_start, state: KVState,
                          q_new, k_new, v_new, active, base: float,
-                         scale: Optional[float] = None, questions=None):
+                         scale: Optional[float] = None, questions=None,
+                         instr: Optional[Instructions] = None):
     """Path 1 for every active question of a ragged batch of prompts.
 
     ctx_k/ctx_v are packed [sum Lc, Hkv, D] with prompt b at
     ctx_start[b]:ctx_start[b+1]; questions of prompt b are
     q_start[b]:q_start[b+1].  The state holds segments *before* this step.
+    With ``instr``, each question's own prompt is [p_s; c_b; segment] for the
+    instruction s that prompt b sits behind.
     Returns out [Nt, Hq, D] and lse [Nt, Hq]; rows of inactive (or
     unrequested) questions are NaN.
     """
@@ -162,9 +183,10 @@ def decode_step_standard(ctx_k, ctx_v, ctx_start, q_start, state: KVState,
             continue
         b = prompt_of[i]
         c0, c1 = ctx_start[b], ctx_start[b + 1]
+        ik, iv = instr.of_prompt(b) if instr is not None else (None, None)
         out[i], lse[i] = standard_prompting_question(
             ctx_k[c0:c1], ctx_v[c0:c1], state.seg_k[i], state.seg_v[i],
-            q_new[i], k_new[i], v_new[i], base, scale)
+            q_new[i], k_new[i], v_new[i], base, scale, instr_k=ik, instr_v=iv)
     return out, lse
 
 
@@ -302,7 +324,8 @@ def stacked_prompt_step(ctx_k, ctx_v, ctx_start, q_start, state: KVState, questi
 # --------------------------------------------------------------------------
 
 def decode_run(ctx_k, ctx_v, ctx_start, q_start, state: KVState, steps_inputs,
-               base: float, scale: Optional[float] = None, record=None):
+               base: float, scale: Optional[float] = None, record=None,
+               instr: Optional[Instructions] = None):
     """Run consecutive decode steps with path 1; returns per-step (out, lse).
 
     ``steps_inputs`` yields (q_new, k_new, v_new, active) per step.  The
@@ -314,6 +337,6 @@ def decode_run(ctx_k, ctx_v, ctx_start, q_start, state: KVState, steps_inputs,
     for t, (q, k, v, act) in enumerate(steps_inputs):
         if record is None or t in record:
             results[t] = decode_step_standard(ctx_k, ctx_v, ctx_start, q_start, state,
-                                              q, k, v, act, base, scale)
+                                              q, k, v, act, base, scale, instr=instr)
         state.append(k, v, act)
     return results

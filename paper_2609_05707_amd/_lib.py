@@ -28,7 +28,7 @@ IPPD_FLAG_SEGMENT_FULL = 1
 IPPD_FLAG_BAD_LAYOUT = 2
 
 EXPORTED = [
-    "ippd_load_context", "ippd_load_segments", "ippd_append_kv",
+    "ippd_load_context", "ippd_load_instructions", "ippd_load_segments", "ippd_append_kv",
     "ippd_decode_workspace_bytes", "standard_decode_workspace_bytes",
     "ippd_decode_attention", "standard_decode_attention",
     "ippd_decode_step", "standard_decode_step",
@@ -60,6 +60,12 @@ class IppdBatch(ctypes.Structure):
         ("seg_len", c_void_p),
         ("active", c_void_p),
         ("err_flag", c_void_p),
+        ("num_instr", c_int32),
+        ("max_instr_len", c_int32),
+        ("max_instr_questions", c_int32),
+        ("instr_start", c_void_p),
+        ("instr_off", c_void_p),
+        ("instr_len", c_void_p),
     ]
 
 
@@ -89,6 +95,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     st = c_int
     lib.ippd_load_context.argtypes = [P(IppdBatch), c_void_p, c_void_p, P(IppdKvCache), c_void_p]
     lib.ippd_load_context.restype = st
+    lib.ippd_load_instructions.argtypes = [P(IppdBatch), c_void_p, c_void_p, P(IppdKvCache), c_void_p]
+    lib.ippd_load_instructions.restype = st
     lib.ippd_load_segments.argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, P(IppdKvCache), c_void_p]
     lib.ippd_load_segments.restype = st
     lib.ippd_append_kv.argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache), c_void_p]
@@ -128,6 +136,11 @@ def _check(fn: str, status: int) -> None:
 def ippd_load_context(batch, k_raw, v_raw, kv, stream) -> None:
     _check("ippd_load_context",
            load_library().ippd_load_context(ctypes.byref(batch), k_raw, v_raw, ctypes.byref(kv), stream))
+
+
+def ippd_load_instructions(batch, k_raw, v_raw, kv, stream) -> None:
+    _check("ippd_load_instructions",
+           load_library().ippd_load_instructions(ctypes.byref(batch), k_raw, v_raw, ctypes.byref(kv), stream))
 
 
 def ippd_load_segments(batch, k_raw, v_raw, init_len, kv, stream) -> None:

@@ -254,47 +254,92 @@ struct UnitLds {
 // its tiles through that XCD's L2) and chunks are dealt to the slices round
 // robin.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW, int NS, bool FUSED, int RB>
+//
+// INSTR: an instruction unit of a two-level batch (attention-only kernel):
+// the group is (instruction s, kv head g), whose rows are the questions of
+// every prompt behind s (or (question i, kv head g) for the baseline), the
+// keys are the instruction's chunk, and the states go to the instruction
+// slots max_chunks + 1 + chunk.  The queries come rotated (q_rot).
+template <typename T, int D, int NW, int NS, bool FUSED, int RB, bool INSTR = false>
 __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char* ring, int wave, int lane) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
   using RL = RowLoads<T, D, FUSED, RB>;
+  static_assert(!(INSTR && FUSED), "instruction units run in the attention-only kernel");
   constexpr int RW = 16 * RB * NW, DPT = RG::BLOCKS / NW;
   constexpr int P0 = RG::NS - 1 < 3 ? RG::NS - 1 : 3;      // tiles issued before the queries are rotated
   const int lr = lane & 15, lg = lane >> 4;
-  const int slice = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int cl = local / p.nrg, rg = local - cl * p.nrg;
+  // instruction units follow the context units (blockIdx >= ctx_blocks)
+  const unsigned ub = INSTR ? blockIdx.x - static_cast<unsigned>(p.ctx_blocks) : blockIdx.x;
+  const int nrg = INSTR ? p.nrg_i : p.nrg;
+  const int nch = INSTR ? p.max_ichunks : p.max_chunks;
+  const int slice = ub & 7, local = ub >> 3;
+  const int cl = local / nrg, rg = local - cl * nrg;
   const int cglob = cl * 8 + slice;
-  if (cglob >= p.n_groups * p.max_chunks) return;
-  const int grp = cglob / p.max_chunks, chunk = cglob - grp * p.max_chunks;
+  if (cglob >= (INSTR ? p.n_igroups : p.n_groups) * nch) return;
+  const int grp = cglob / nch, chunk = cglob - grp * nch;
 
   int b, g, qa, qb;
-  if (p.shared) {
-    g = grp / p.B;
-    b = grp - g * p.B;
-  } else {
-    g = grp / p.Nt;
-    qa = grp - g * p.Nt;
-    b = find_prompt(p, qa, lane).b;
-    if (b >= p.B) {
-      if (threadIdx.x == 0 && chunk == 0) raise_flag(p.err_flag, kFlagBadLayout);
+  int ctx_len, slot_k;                             // key-range length; slot index of this chunk's states
+  int64_t off;                                     // key-range start in the pool
+  if constexpr (INSTR) {
+    int s = 0;
+    bool ok;
+    if (p.shared) {
+      g = grp / p.S;
+      s = grp - g * p.S;
+      const int pa = p.instr_start[s], pe = p.instr_start[s + 1];
+      // the instructions' prompt ranges must tile [0, B) so that every
+      // question's instruction slots are written
+      ok = pa >= 0 && pe >= pa && pe <= p.B && (s > 0 || pa == 0) && (s < p.S - 1 || pe == p.B);
+      qa = ok ? p.q_start[pa] : 0;
+      qb = ok ? p.q_start[pe] : 0;
+      ok = ok && qa >= 0 && qb >= qa && qb <= p.Nt && qb - qa <= p.max_instr_questions;
+    } else {
+      g = grp / p.Nt;
+      qa = grp - g * p.Nt;
+      qb = qa + 1;
+      b = find_prompt(p, qa, lane).b;
+      ok = b < p.B;
+      if (ok) s = instr_of_prompt(p.instr_start, p.S, b);
+    }
+    off = ok ? p.instr_off[s] : 0;
+    ctx_len = ok ? p.instr_len[s] : 0;
+    if (!ok || off < 0 || (off & 7) != 0 || ctx_len < 0 || ctx_len > p.max_instr_len || off + ctx_len > p.pool) {
+      if (threadIdx.x == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
       return;
     }
-  }
-  if (!prompt_layout_ok(p, b)) {
-    if (threadIdx.x == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
-    return;
-  }
-  if (p.shared) {
-    qa = p.q_start[b];
-    qb = p.q_start[b + 1];
+    slot_k = p.max_chunks + 1 + chunk;
   } else {
-    qb = qa + 1;
+    if (p.shared) {
+      g = grp / p.B;
+      b = grp - g * p.B;
+    } else {
+      g = grp / p.Nt;
+      qa = grp - g * p.Nt;
+      b = find_prompt(p, qa, lane).b;
+      if (b >= p.B) {
+        if (threadIdx.x == 0 && chunk == 0) raise_flag(p.err_flag, kFlagBadLayout);
+        return;
+      }
+    }
+    if (!prompt_layout_ok(p, b)) {
+      if (threadIdx.x == 0 && chunk == 0 && rg == 0) raise_flag(p.err_flag, kFlagBadLayout);
+      return;
+    }
+    if (p.shared) {
+      qa = p.q_start[b];
+      qb = p.q_start[b + 1];
+    } else {
+      qb = qa + 1;
+    }
+    ctx_len = p.ctx_len[b];
+    off = p.ctx_off[b];
+    slot_k = chunk;
   }
   const int G = p.G;
   const int nrows = (qb - qa) * G;
   const int row0 = rg * RW;
-  const int ctx_len = p.ctx_len[b];
   if (row0 >= nrows) return;
   if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len) {
     // past the prompt's context: an empty state (max -inf) for each row, so
@@ -304,7 +349,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
       for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + 16 * (RB * wave + rb) + lr;
         if (row < nrows) {
-          const int64_t slot = (static_cast<int64_t>(chunk) * p.Nt + qa + row / G) * p.Hq + g * G + row % G;
+          const int64_t slot = (static_cast<int64_t>(slot_k) * p.Nt + qa + row / G) * p.Hq + g * G + row % G;
           *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, 0.f);
         }
       }
@@ -312,7 +357,6 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     return;
   }
 
-  const int64_t off = p.ctx_off[b];
   const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
   const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
   const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
@@ -419,7 +463,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(chunk) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
+    if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(slot_k) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
   }
 }
 
@@ -686,8 +730,14 @@ __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepPa
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int blk = static_cast<int>(blockIdx.x);
-  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
-  else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks, wave, lane);
+  if (blk < p.ctx_blocks) {
+    context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
+  } else if constexpr (FUSED) {
+    segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks, wave, lane);
+  } else {
+    if (blk < p.ctx_blocks + p.instr_blocks) context_unit<T, D, NW, NS, false, RB, true>(p, sh.main, wave, lane);
+    else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks - p.instr_blocks, wave, lane);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -736,7 +786,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
   const int tid = threadIdx.x;
   const int P = p.merge_phases, per = kMergeThreads / P;
   const int i = blockIdx.x / p.merge_parts, part = blockIdx.x - i * p.merge_parts;
-  const int nslot = p.max_chunks + 1;              // chunks, then the segment
+  const int nslot = p.max_chunks + 1 + p.max_ichunks;   // context chunks, the segment, instruction chunks
   const float c = p.c;
   const int items = p.Hq * (D / 8);
   const int f = tid / per, local = tid - f * per;

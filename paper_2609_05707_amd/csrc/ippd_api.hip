@@ -38,7 +38,22 @@ ippd_status_t check_batch(const ippd_batch_t* bt) {
   if (!isfinite(bt->scale)) return IPPD_ERR_SHAPE;
   if (!bt->ctx_off || !bt->ctx_len || !bt->q_start || !bt->seg_len || !bt->active || !bt->err_flag)
     return IPPD_ERR_NULL;
+  if (bt->num_instr < 0) return IPPD_ERR_SHAPE;
+  if (bt->num_instr > 0) {
+    if (bt->num_instr > bt->num_prompts || bt->max_instr_len < 0 || bt->max_instr_len > bt->ctx_pool_tokens ||
+        bt->max_instr_questions < 1)
+      return IPPD_ERR_SHAPE;
+    if (!bt->instr_start || !bt->instr_off || !bt->instr_len) return IPPD_ERR_NULL;
+  }
   return IPPD_OK;
+}
+
+// Two-level fields of the kernel parameter blocks (S = 0 leaves positions unshifted).
+template <typename P>
+void set_instr_positions(const ippd_batch_t* bt, P* p) {
+  p->S = bt->num_instr;
+  p->instr_start = bt->num_instr > 0 ? bt->instr_start : nullptr;
+  p->instr_len = bt->num_instr > 0 ? bt->instr_len : nullptr;
 }
 
 float softmax_scale(const ippd_batch_t* bt) {
@@ -90,9 +105,14 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   const int wg_per_cu = (rb == 2 && waves == 8) ? 1 : 2;
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
+  // two-level batch: instruction groups, (instruction, kv head) or (question, kv head)
+  const int S = bt->num_instr;
+  const int64_t n_igroups = S == 0 ? 0 : (shared ? static_cast<int64_t>(S) : bt->num_questions) * bt->num_kv_heads;
+  const int64_t irows = shared ? static_cast<int64_t>(bt->max_instr_questions) * G : G;
+  const int nrg_i = S == 0 ? 1 : static_cast<int>((irows + 16 * rb * waves - 1) / (16 * rb * waves));
   int chunk = bt->chunk_tokens;
   if (chunk == 0) {
-    const int64_t work = n_groups * nrg * bt->max_ctx_len;
+    const int64_t work = n_groups * nrg * bt->max_ctx_len + n_igroups * nrg_i * (S ? bt->max_instr_len : 0);
     const int64_t target = static_cast<int64_t>(compute_units()) * wg_per_cu;
     int64_t ch = (work + target - 1) / target;
     ch = (ch + 31) / 32 * 32;
@@ -101,19 +121,21 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   }
   const int64_t max_chunks = (bt->max_ctx_len + chunk - 1) / chunk;
   const int64_t ctx_blocks = 8 * nrg * ((n_groups * max_chunks + 7) / 8);
+  const int64_t max_ichunks = S == 0 ? 0 : (bt->max_instr_len + chunk - 1) / chunk;
+  const int64_t instr_blocks = 8 * nrg_i * ((n_igroups * max_ichunks + 7) / 8);
   // segment tasks (question, kv head): as few per unit as keeps the segment
   // units within one round of resident workgroups (they run after the
   // context units), at most `waves` per unit, and all tasks' wave states
   // must fit the smallest LDS ring (32 KB)
-  const bool deep = ctx_blocks <= compute_units() || wg_per_cu == 1;
+  const bool deep = ctx_blocks + instr_blocks <= compute_units() || wg_per_cu == 1;
   const int64_t slots = static_cast<int64_t>(compute_units()) * (deep ? 1 : 2);
   const int64_t seg_tasks = static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   const int64_t state_bytes = static_cast<int64_t>(G) * (bt->head_dim + 4) * 4;
   int tpu = 1;
   while (tpu < waves && (seg_tasks + tpu - 1) / tpu > slots && 2 * tpu * state_bytes <= 32768) tpu *= 2;
   const int64_t seg_blocks = (seg_tasks + tpu - 1) / tpu;
-  const int64_t grid = ctx_blocks + seg_blocks;
-  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30)) return false;
+  const int64_t grid = ctx_blocks + instr_blocks + seg_blocks;
+  if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) || n_igroups * max_ichunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
   pl->rb = rb;
@@ -126,7 +148,11 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->seg_blocks = static_cast<int>(seg_blocks);
   pl->seg_tpu = tpu;
   pl->deep = deep ? 1 : 0;
-  pl->part_slots = static_cast<size_t>(max_chunks + 1) * bt->num_questions * bt->num_q_heads;
+  pl->n_igroups = static_cast<int>(n_igroups);
+  pl->nrg_i = nrg_i;
+  pl->max_ichunks = static_cast<int>(max_ichunks);
+  pl->instr_blocks = static_cast<int>(instr_blocks);
+  pl->part_slots = static_cast<size_t>(max_chunks + 1 + max_ichunks) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = 0;
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));
@@ -151,6 +177,15 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   if (st != IPPD_OK) return st;
   if (!kv || !out || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt) return IPPD_ERR_NULL;
   if (fused ? (!q_new || !k_new || !v_new) : !q_rot_in) return IPPD_ERR_NULL;
+  if (fused && bt->num_instr > 0) {
+    // two-level batch: the instruction units take rotated queries, so the step
+    // runs as the append launch followed by the attention launches
+    if (!q_rot_out) return IPPD_ERR_NULL;
+    ippd_status_t a = ippd_append_kv(bt, q_new, k_new, v_new, q_rot_out, kv, stream);
+    if (a != IPPD_OK) return a;
+    return decode(bt, shared, false, nullptr, nullptr, nullptr, q_rot_out, nullptr, kv, out, lse, workspace,
+                  workspace_bytes, stream);
+  }
   if (!aligned16(out) || !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) ||
       !aligned16(kv->seg_vt) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3)))
     return IPPD_ERR_ALIGN;
@@ -180,11 +215,16 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.shared = pl.shared; p.fused = fused ? 1 : 0; p.nrg = pl.nrg; p.chunk = pl.chunk;
   p.max_chunks = pl.max_chunks; p.n_groups = pl.n_groups; p.ctx_blocks = pl.ctx_blocks;
   p.seg_tpu = pl.seg_tpu;
+  p.instr_start = bt->num_instr > 0 ? bt->instr_start : nullptr;
+  p.instr_off = bt->num_instr > 0 ? bt->instr_off : nullptr;
+  p.instr_len = bt->num_instr > 0 ? bt->instr_len : nullptr;
+  p.S = bt->num_instr; p.max_instr_len = bt->max_instr_len; p.max_instr_questions = bt->max_instr_questions;
+  p.n_igroups = pl.n_igroups; p.nrg_i = pl.nrg_i; p.max_ichunks = pl.max_ichunks; p.instr_blocks = pl.instr_blocks;
   // merge: enough threads per item that each folds at most 8 of the
   // max_chunks + 1 partial states; items split over workgroups of 512
   {
     int ph = 1;
-    while (ph < 8 && (pl.max_chunks + 1 + ph - 1) / ph > 8) ph *= 2;
+    while (ph < 8 && (pl.max_chunks + 1 + pl.max_ichunks + ph - 1) / ph > 8) ph *= 2;
     const int items = bt->num_q_heads * (bt->head_dim / 8);
     const int per = 512 / ph;
     p.merge_phases = ph;
@@ -234,6 +274,7 @@ ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens,
   if (!aligned16(q_ctx) || !aligned16(q_seg) || !aligned16(out_ctx) || !aligned16(out_seg) ||
       !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) || !aligned16(kv->seg_vt))
     return IPPD_ERR_ALIGN;
+  if (bt->num_instr > 0) return IPPD_ERR_SHAPE;    // the prefill has no instruction level
   ippd::PrefillPlan pl;
   if (!plan_prefill(bt, shared, max_q_tokens, &pl)) return IPPD_ERR_SHAPE;
   if (pl.grid == 0) return IPPD_OK;
@@ -270,6 +311,26 @@ ippd_status_t ippd_load_context(const ippd_batch_t* bt, const void* k_raw, const
   p.ctx_off = bt->ctx_off; p.ctx_len = bt->ctx_len; p.err_flag = bt->err_flag;
   p.pool = bt->ctx_pool_tokens; p.B = bt->num_prompts; p.Hkv = bt->num_kv_heads; p.D = bt->head_dim;
   p.max_ctx_len = bt->max_ctx_len;
+  set_instr_positions(bt, &p);
+  fill_inv_freq(bt, p.inv_freq);
+  return hip_status(ippd::launch_load_context(bt->dtype, p, stream));
+}
+
+ippd_status_t ippd_load_instructions(const ippd_batch_t* bt, const void* k_raw, const void* v_raw,
+                                     const ippd_kv_cache_t* kv, hipStream_t stream) {
+  ippd_status_t st = check_batch(bt);
+  if (st != IPPD_OK) return st;
+  if (bt->num_instr == 0) return IPPD_ERR_SHAPE;
+  if (!k_raw || !v_raw || !kv || !kv->ctx_k || !kv->ctx_vt) return IPPD_ERR_NULL;
+  if (!aligned16(k_raw) || !aligned16(v_raw) || !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt))
+    return IPPD_ERR_ALIGN;
+  // the context loader over the instruction blocks, at positions 0..len-1
+  ippd::LoadContextParams p;
+  p.k_raw = k_raw; p.v_raw = v_raw; p.ctx_k = kv->ctx_k; p.ctx_vt = kv->ctx_vt;
+  p.ctx_off = bt->instr_off; p.ctx_len = bt->instr_len; p.err_flag = bt->err_flag;
+  p.pool = bt->ctx_pool_tokens; p.B = bt->num_instr; p.Hkv = bt->num_kv_heads; p.D = bt->head_dim;
+  p.max_ctx_len = bt->max_instr_len;
+  p.S = 0; p.instr_start = nullptr; p.instr_len = nullptr;
   fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_load_context(bt->dtype, p, stream));
 }
@@ -287,6 +348,7 @@ ippd_status_t ippd_load_segments(const ippd_batch_t* bt, const void* k_raw, cons
   p.ctx_len = bt->ctx_len; p.q_start = bt->q_start; p.seg_len = bt->seg_len; p.err_flag = bt->err_flag;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hkv = bt->num_kv_heads; p.D = bt->head_dim;
   p.seg_cap = bt->seg_capacity;
+  set_instr_positions(bt, &p);
   fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_load_segments(bt->dtype, p, stream));
 }
@@ -307,6 +369,7 @@ ippd_status_t ippd_append_kv(const ippd_batch_t* bt, const void* q_new, const vo
   p.active = bt->active; p.err_flag = bt->err_flag;
   p.B = bt->num_prompts; p.Nt = bt->num_questions; p.Hq = bt->num_q_heads; p.Hkv = bt->num_kv_heads;
   p.D = bt->head_dim; p.seg_cap = bt->seg_capacity;
+  set_instr_positions(bt, &p);
   fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_append(bt->dtype, p, stream));
 }

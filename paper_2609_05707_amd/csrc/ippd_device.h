@@ -110,6 +110,24 @@ __device__ __forceinline__ int prompt_of(const int32_t* q_start, int B, int i) {
   return lo;
 }
 
+// Virtual position of prompt b's first context token: the length of the
+// instruction it sits behind in a two-level batch (the largest s with
+// instr_start[s] <= b), 0 without an instruction level.
+// Instruction of prompt b in a two-level batch: the largest s in [0, S) with
+// instr_start[s] <= b.
+__device__ __forceinline__ int instr_of_prompt(const int32_t* instr_start, int S, int b) {
+  int lo = 0, hi = S - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (instr_start[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int64_t instr_pos_base(const int32_t* instr_start, const int32_t* instr_len, int S, int b) {
+  return S > 0 ? instr_len[instr_of_prompt(instr_start, S, b)] : 0;
+}
+
 __device__ __forceinline__ void raise_flag(int32_t* err_flag, int bits) {
   atomicOr(reinterpret_cast<int*>(err_flag), bits);
 }

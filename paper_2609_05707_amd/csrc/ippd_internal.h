@@ -15,6 +15,7 @@ struct LoadContextParams {
   const void* k_raw; const void* v_raw;     // [pool][Hkv][D]
   void* ctx_k; void* ctx_vt;
   const int64_t* ctx_off; const int32_t* ctx_len; int32_t* err_flag;
+  const int32_t* instr_start; const int32_t* instr_len; int S;   // two-level batch: position base (S = 0: none)
   int64_t pool; int B, Hkv, D, max_ctx_len;
   double inv_freq[kMaxHalfDim];
 };
@@ -24,6 +25,7 @@ struct LoadSegmentsParams {
   const int32_t* init_len;
   void* seg_k; void* seg_vt;
   const int32_t* ctx_len; const int32_t* q_start; int32_t* seg_len; int32_t* err_flag;
+  const int32_t* instr_start; const int32_t* instr_len; int S;   // two-level batch: position base (S = 0: none)
   int B, Nt, Hkv, D, seg_cap;
   double inv_freq[kMaxHalfDim];
 };
@@ -33,6 +35,7 @@ struct AppendParams {
   void* q_rot; void* seg_k; void* seg_vt;
   const int32_t* ctx_len; const int32_t* q_start;
   int32_t* seg_len; const uint8_t* active; int32_t* err_flag;
+  const int32_t* instr_start; const int32_t* instr_len; int S;   // two-level batch: position base (S = 0: none)
   int B, Nt, Hq, Hkv, D, seg_cap;
   double inv_freq[kMaxHalfDim];
 };
@@ -54,7 +57,12 @@ struct StepPlan {
   int seg_blocks;          // segment units: ceil(Nt * Hkv / seg_tpu)
   int seg_tpu;             // segment tasks per unit (power of two dividing waves)
   int deep;                // 1: deep LDS ring (the context units fit the chip in one wave)
-  size_t part_slots;       // (max_chunks + 1) * Nt * Hq partial softmax states (chunks, segment)
+  int n_igroups;           // instruction groups: (instruction s, kv head g) or (question i, kv head g)
+  int nrg_i;               // row groups per instruction group
+  int max_ichunks;         // ceil(max_instr_len / chunk)
+  int instr_blocks;        // instruction units, after the context units
+  size_t part_slots;       // (max_chunks + 1 + max_ichunks) * Nt * Hq partial softmax states
+                           // (context chunks, segment, instruction chunks)
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
   size_t workspace_bytes;
 };
@@ -101,6 +109,9 @@ struct StepParams {
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len, max_questions;
   int shared, fused, nrg, chunk, max_chunks, n_groups, ctx_blocks, seg_tpu;
+  // two-level batch: instruction units (blocks ctx_blocks .. ctx_blocks + instr_blocks - 1)
+  const int32_t* instr_start; const int64_t* instr_off; const int32_t* instr_len;
+  int S, max_instr_len, max_instr_questions, n_igroups, nrg_i, max_ichunks, instr_blocks;
   int merge_phases;        // threads per merged item (slots split among them), power of 2
   int merge_parts;         // merge workgroups per question
   float c;                 // scale * log2(e)

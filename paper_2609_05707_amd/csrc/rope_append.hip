@@ -3,7 +3,8 @@
 // Positions follow the virtual-position rule of Sec. 4.1: a context token t
 // sits at t (instruction folded into the context), segment slot t of a
 // question of prompt b at ctx_len[b] + t, and the token fed at a decode step
-// at ctx_len[b] + seg_len[i].  theta_j = base^(-2j/D) comes from the host in
+// at ctx_len[b] + seg_len[i]; behind an instruction of a two-level batch all
+// of them move up by its length.  theta_j = base^(-2j/D) comes from the host in
 // fp64; cos/sin use the fp64-reduced angle (rope_cos_sin).
 #include "ippd_device.h"
 #include "ippd_internal.h"
@@ -42,7 +43,7 @@ __global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
     return;
   }
   const int D = p.D, half = D / 2;
-  const int64_t pos = static_cast<int64_t>(p.ctx_len[b]) + s;
+  const int64_t pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b) + p.ctx_len[b] + s;
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
     float c, sn;
     rope_cos_sin(pos, p.inv_freq[j], c, sn);
@@ -100,6 +101,7 @@ __global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, 
   if (t0 >= len) return;
   const int nt = min(kLoadTile, len - t0);
   const int D = p.D, half = D / 2;
+  const int64_t base_pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b);
   const T* __restrict__ kr = static_cast<const T*>(p.k_raw);
   const T* __restrict__ vr = static_cast<const T*>(p.v_raw);
   T* __restrict__ ck = static_cast<T*>(p.ctx_k);
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(256) void load_context_kernel(LoadContextParams p, 
     const int tt = e / half, j = e - tt * half;
     const int t = t0 + tt;
     float c, sn;
-    rope_cos_sin(t, p.inv_freq[j], c, sn);
+    rope_cos_sin(base_pos + t, p.inv_freq[j], c, sn);
     const int64_t src = ((off + t) * p.Hkv + g) * D;
     const int64_t dst = (static_cast<int64_t>(g) * p.pool + off + t) * D;
     float x, y;
@@ -148,7 +150,7 @@ __global__ __launch_bounds__(256) void load_segments_kernel(LoadSegmentsParams p
   if (t0 >= n) return;
   const int nt = min(kLoadTile, n - t0);
   const int D = p.D, half = D / 2;
-  const int64_t base_pos = p.ctx_len[b];
+  const int64_t base_pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b) + p.ctx_len[b];
   const T* __restrict__ kr = static_cast<const T*>(p.k_raw);
   const T* __restrict__ vr = static_cast<const T*>(p.v_raw);
   T* __restrict__ sk = static_cast<T*>(p.seg_k);

@@ -34,7 +34,11 @@ class DecodeBatch:
     def __init__(self, ctx_len: Sequence[int], q_count: Sequence[int], hq: int, hkv: int,
                  head_dim: int, dtype: str, seg_capacity: int, rope_base: float = 10000.0,
                  scale: float = 0.0, chunk_tokens: int = 0, max_questions: Optional[int] = None,
-                 layers: int = 1, tile_rows: int = 0, device: str = "cuda"):
+                 layers: int = 1, tile_rows: int = 0, device: str = "cuda",
+                 instr_len: Optional[Sequence[int]] = None, instr_prompt_start: Optional[Sequence[int]] = None):
+        """instr_len / instr_prompt_start (optional) make a two-level batch:
+        prompts instr_prompt_start[s] .. instr_prompt_start[s+1]-1 sit behind
+        instruction s of instr_len[s] tokens, held at the front of the pool."""
         self.device = torch.device(device)
         self.dtype = dtype
         self.tdtype = torch_dtype(dtype)
@@ -45,9 +49,14 @@ class DecodeBatch:
         self.hq, self.hkv, self.D = hq, hkv, head_dim
         self.seg_cap = _round8(max(seg_capacity, 8))
         self.layers = layers
+        self.S = 0 if instr_len is None else len(instr_len)
+        self.instr_len = np.asarray(instr_len if instr_len is not None else [], dtype=np.int64)
+        ipad = np.array([_round8(x) for x in self.instr_len], dtype=np.int64)
+        self.instr_off = np.concatenate([[0], np.cumsum(ipad)[:-1]]).astype(np.int64) if self.S else ipad
+        ibase = int(ipad.sum())
         padded = np.array([_round8(x) for x in self.ctx_len], dtype=np.int64)
-        self.ctx_off = np.concatenate([[0], np.cumsum(padded)[:-1]]).astype(np.int64)
-        self.pool = max(8, int(padded.sum()))
+        self.ctx_off = ibase + np.concatenate([[0], np.cumsum(padded)[:-1]]).astype(np.int64)
+        self.pool = max(8, ibase + int(padded.sum()))
         self.q_start = np.concatenate([[0], np.cumsum(self.q_count)]).astype(np.int32)
         self.max_ctx_len = int(self.ctx_len.max()) if self.B else 0
         self.max_questions = int(max_questions if max_questions is not None
@@ -58,6 +67,16 @@ class DecodeBatch:
         self.d_q_start = torch.from_numpy(self.q_start).to(dev)
         self.d_active = torch.ones(max(self.Nt, 1), dtype=torch.uint8, device=dev)
         self.d_err = torch.zeros(1, dtype=torch.int32, device=dev)
+        if self.S:
+            self.instr_prompt_start = np.asarray(instr_prompt_start, dtype=np.int32)
+            if len(self.instr_prompt_start) != self.S + 1:
+                raise ValueError("instr_prompt_start needs num_instr + 1 entries")
+            self.max_instr_questions = max(1, max(int(self.q_start[self.instr_prompt_start[s + 1]] -
+                                                      self.q_start[self.instr_prompt_start[s]])
+                                                  for s in range(self.S)))
+            self.d_instr_start = torch.from_numpy(self.instr_prompt_start).to(dev)
+            self.d_instr_off = torch.from_numpy(self.instr_off).to(dev)
+            self.d_instr_len = torch.from_numpy(self.instr_len.astype(np.int32)).to(dev)
         self.seg_len = [torch.zeros(max(self.Nt, 1), dtype=torch.int32, device=dev) for _ in range(layers)]
         td = self.tdtype
         self.ctx_k = [torch.empty(hkv, self.pool, head_dim, dtype=td, device=dev) for _ in range(layers)]
@@ -91,6 +110,13 @@ class DecodeBatch:
             bt.seg_len = self.seg_len[layer].data_ptr()
             bt.active = self.d_active.data_ptr()
             bt.err_flag = self.d_err.data_ptr()
+            if self.S:
+                bt.num_instr = self.S
+                bt.max_instr_len = int(self.instr_len.max())
+                bt.max_instr_questions = self.max_instr_questions
+                bt.instr_start = self.d_instr_start.data_ptr()
+                bt.instr_off = self.d_instr_off.data_ptr()
+                bt.instr_len = self.d_instr_len.data_ptr()
             self.batches.append(bt)
             kv = L.IppdKvCache()
             kv.ctx_k = self.ctx_k[layer].data_ptr()
@@ -147,6 +173,21 @@ class DecodeBatch:
                             self.caches[layer], self.stream())
         torch.cuda.current_stream().synchronize()
 
+    def load_instructions(self, layer: int, k_packed, v_packed) -> None:
+        """k/v_packed: [sum instr_len, Hkv, D] raw (pre-rotation), instructions in order."""
+        kp, vp = self.to_dev(k_packed), self.to_dev(v_packed)
+        k_raw = torch.zeros(self.pool, self.hkv, self.D, dtype=self.tdtype, device=self.device)
+        v_raw = torch.zeros_like(k_raw)
+        src = 0
+        for s in range(self.S):
+            n, o = int(self.instr_len[s]), int(self.instr_off[s])
+            k_raw[o:o + n] = kp[src:src + n]
+            v_raw[o:o + n] = vp[src:src + n]
+            src += n
+        L.ippd_load_instructions(self.batches[layer], k_raw.data_ptr(), v_raw.data_ptr(),
+                                 self.caches[layer], self.stream())
+        torch.cuda.current_stream().synchronize()
+
     def load_segments(self, layer: int, k_packed, v_packed, seg_len0) -> None:
         """k/v_packed: [sum seg_len0, Hkv, D] raw; question i owns the next seg_len0[i] rows."""
         seg_len0 = np.asarray(seg_len0, dtype=np.int64)
@@ -201,7 +242,7 @@ class DecodeBatch:
         q_rot = self.q_rot if q_rot is None else q_rot
         out = self.out if out is None else out
         lse = self.lse if lse is None else lse
-        qr = q_rot.data_ptr() if write_q_rot else None
+        qr = q_rot.data_ptr() if (write_q_rot or self.S) else None   # a two-level step needs q_rot
         lse_ptr = lse.data_ptr() if with_lse else None
         fn = L.standard_decode_step if standard else L.ippd_decode_step
         ws, wsb = (self.ws_std, self.ws_std_bytes) if standard else (self.ws_ippd, self.ws_ippd_bytes)

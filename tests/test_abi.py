@@ -169,3 +169,38 @@ def test_prefill_validation(lib):
         assert call(kv=kv_cache(MISALIGNED)) == L.IPPD_ERR_ALIGN
         assert call(m=-1) == L.IPPD_ERR_SHAPE
     assert lib.ippd_version() >= 500
+
+
+def test_instruction_level_validation(lib):
+    kv = kv_cache()
+    bad = [(dict(num_instr=-1), L.IPPD_ERR_SHAPE),
+           (dict(num_instr=2), L.IPPD_ERR_SHAPE),                       # more instructions than prompts
+           (dict(num_instr=1, max_instr_len=8, max_instr_questions=0), L.IPPD_ERR_SHAPE),
+           (dict(num_instr=1, max_instr_len=300, max_instr_questions=4), L.IPPD_ERR_SHAPE),   # beyond the pool
+           (dict(num_instr=1, max_instr_len=8, max_instr_questions=4), L.IPPD_ERR_NULL)]      # arrays missing
+    for kw, status in bad:
+        bt = valid_batch(**kw)
+        assert decode_status(lib, bt) == status, kw
+        assert lib.ippd_load_instructions(ctypes.byref(bt), FAKE, FAKE, ctypes.byref(kv), None) == status, kw
+    bt = valid_batch()
+    assert lib.ippd_load_instructions(ctypes.byref(bt), FAKE, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_SHAPE
+    good = valid_batch(num_instr=1, max_instr_len=64, max_instr_questions=4, instr_start=FAKE, instr_off=FAKE,
+                       instr_len=FAKE)
+    assert lib.ippd_load_instructions(ctypes.byref(good), None, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_NULL
+    assert lib.ippd_prefill_attention(ctypes.byref(good), 8, FAKE, FAKE, ctypes.byref(kv), FAKE, FAKE,
+                                      None) == L.IPPD_ERR_SHAPE
+    # the fused step of a two-level batch needs q_rot (it runs the append first)
+    args = (ctypes.byref(good), FAKE, FAKE, FAKE, None, ctypes.byref(kv), FAKE, None, FAKE, 1 << 30, None)
+    assert lib.ippd_decode_step(*args) == L.IPPD_ERR_NULL
+
+
+def test_workspace_formula_with_instructions(lib):
+    # (max_chunks + 1 + max_ichunks) * Nt * Hq partial states: context chunks,
+    # the segment, then instruction chunks
+    bt = valid_batch(chunk_tokens=64, num_instr=1, max_instr_len=100, max_instr_questions=4, instr_start=FAKE,
+                     instr_off=FAKE, instr_len=FAKE)
+    slots = (256 // 64 + 1 + 2) * 4 * 4
+    r = lambda x: (x + 255) // 256 * 256
+    want = r(slots * 64 * 4) + r(slots * 2 * 4)
+    assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == want
+    assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == want

@@ -182,6 +182,38 @@ def test_ippd_masked_prompt_equals_standard_prompting(seed, lp):
         np.testing.assert_allclose(l2[i], l1, atol=1e-12)
 
 
+def test_two_level_batch_matches_stacked_prompts():
+    """Two-level batch (Sec. 4.4): prompts 0-1 behind instruction 0 and prompt 2
+    behind instruction 1.  The per-question oracle with per-prompt
+    instructions equals, for each instruction, the literal stacked prompt of
+    that instruction and its contexts under the dense mask."""
+    c = _small_case(31, B=3)
+    r = rng(32)
+    hkv, d = 2, 16
+    lps = [4, 3]
+    ik = [r.standard_normal((n, hkv, d)) for n in lps]
+    iv = [r.standard_normal((n, hkv, d)) for n in lps]
+    instr = O.Instructions(np.array([0, 2, 3]), np.array([0, 4, 7]), np.concatenate(ik), np.concatenate(iv))
+    nt = len(c["seg_len"])
+    act = np.ones(nt, bool)
+    act[-1] = False
+    out, lse = O.decode_step_standard(c["ck"], c["cv"], c["ctx_start"], c["q_start"],
+                                      O.KVState(list(c["sk"]), list(c["sv"])), c["q"], c["k"], c["v"], act,
+                                      1e4, instr=instr)
+    for s, (b0, b1) in enumerate([(0, 2), (2, 3)]):
+        q0, q1 = c["q_start"][b0], c["q_start"][b1]
+        cs = c["ctx_start"][b0:b1 + 1] - c["ctx_start"][b0]
+        qs = c["q_start"][b0:b1 + 1] - q0
+        ctx = slice(c["ctx_start"][b0], c["ctx_start"][b1])
+        st = O.KVState(list(c["sk"][q0:q1]), list(c["sv"][q0:q1]))
+        o2, l2 = O.stacked_prompt_step(c["ck"][ctx], c["cv"][ctx], cs, qs, st, c["seg_len"][q0:q1],
+                                       c["q"][q0:q1], c["k"][q0:q1], c["v"][q0:q1], act[q0:q1], 1e4,
+                                       instr_k=ik[s], instr_v=iv[s])
+        np.testing.assert_allclose(np.nan_to_num(out[q0:q1]), np.nan_to_num(o2), atol=1e-12)
+        np.testing.assert_allclose(np.nan_to_num(lse[q0:q1]), np.nan_to_num(l2), atol=1e-12)
+    assert np.isnan(out[-1]).all()
+
+
 def test_batched_step_matches_per_question():
     c = _small_case(20, B=3)
     nt = len(c["seg_len"])

@@ -18,7 +18,9 @@ still-decoding questions (Sec. 4.4).  The synthetic recipe, per workload:
   raw segment K, segment V, in that order, ``standard_normal * value_std``;
 * step stream ``default_rng([wid, 2, layer, step])``: q_new, k_new, v_new;
 * prefill stream ``default_rng([wid, 3, layer])``: raw queries of every
-  context token, then of every segment token (the rows of a prefill).
+  context token, then of every segment token (the rows of a prefill);
+* two-level batches: instruction lengths from ``default_rng([wid, 4])``,
+  raw instruction K then V from ``default_rng([wid, 5, layer])``.
 
 Values are drawn as float32; bf16 workloads are then rounded to the nearest
 bf16 value (ties to even) and kept as float32 arrays holding bf16 values.
@@ -40,6 +42,7 @@ __all__ = [
     "layer_kv",
     "step_inputs",
     "prefill_queries",
+    "instructions",
     "round_to_bf16",
     "bf16_bits",
 ]
@@ -235,3 +238,32 @@ def prefill_queries(st: Structure, layer: int = 0) -> PrefillQueries:
     cq = _draw(rng, (int(st.ctx_start[-1]), wl.hq, wl.head_dim), wl)
     sq = _draw(rng, (int(st.seg_start[-1]), wl.hq, wl.head_dim), wl)
     return PrefillQueries(cq, sq)
+
+
+@dataclass
+class InstructionKV:
+    """Instruction blocks of a two-level batch: prompts prompt_start[s] ..
+    prompt_start[s+1]-1 sit behind instruction s of lp[s] tokens, whose raw
+    keys/values are k/v[tok_start[s]:tok_start[s+1]]."""
+
+    prompt_start: np.ndarray   # [S+1]
+    lp: np.ndarray             # [S]
+    tok_start: np.ndarray      # [S+1]
+    k: np.ndarray              # [sum lp, Hkv, D]
+    v: np.ndarray
+
+
+def instructions(st: Structure, contexts_per_instr: int, lp: Tuple[int, int], layer: int = 0) -> InstructionKV:
+    """Consecutive prompts grouped contexts_per_instr at a time (the last group
+    may be smaller) behind instructions of U{lp} tokens."""
+    wl = st.wl
+    B = wl.num_prompts
+    prompt_start = np.array(list(range(0, B, contexts_per_instr)) + [B], dtype=np.int64)
+    S = len(prompt_start) - 1
+    lens = np.random.default_rng([wl.wid, 4]).integers(lp[0], lp[1], size=S, endpoint=True).astype(np.int64)
+    tok_start = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    rng = np.random.default_rng([wl.wid, 5, layer])
+    shape = (int(tok_start[-1]), wl.hkv, wl.head_dim)
+    k = _draw(rng, shape, wl)
+    v = _draw(rng, shape, wl)
+    return InstructionKV(prompt_start, lens, tok_start, k, v)
