@@ -246,9 +246,7 @@ ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q
  * q_rot [Nt][Hq][D] receives the rotated queries, or may be NULL.  An active
  * question whose segment is full (seg_len[i] == seg_capacity) sets
  * IPPD_FLAG_SEGMENT_FULL and gets no output row.  workspace as for
- * ippd_decode_attention.  In a two-level batch the call runs
- * ippd_append_kv and ippd_decode_attention as three launches (q_rot is then
- * required).
+ * ippd_decode_attention.
  */
 ippd_status_t ippd_decode_step(const ippd_batch_t *batch, const void *q_new, const void *k_new,
                                const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,

@@ -255,17 +255,17 @@ struct UnitLds {
 // robin.
 // ---------------------------------------------------------------------------
 //
-// INSTR: an instruction unit of a two-level batch (attention-only kernel):
-// the group is (instruction s, kv head g), whose rows are the questions of
-// every prompt behind s (or (question i, kv head g) for the baseline), the
-// keys are the instruction's chunk, and the states go to the instruction
-// slots max_chunks + 1 + chunk.  The queries come rotated (q_rot).
+// INSTR: an instruction unit of a two-level batch: the group is
+// (instruction s, kv head g), whose rows are the questions of every prompt
+// behind s (or (question i, kv head g) for the baseline), the keys are the
+// instruction's chunk, and the states go to the instruction slots
+// max_chunks + 1 + chunk.  In the fused step each row's query is rotated at
+// its own question's position instr_len[s] + ctx_len[b] + seg_len[i].
 template <typename T, int D, int NW, int NS, bool FUSED, int RB, bool INSTR = false>
 __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char* ring, int wave, int lane) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
   using RL = RowLoads<T, D, FUSED, RB>;
-  static_assert(!(INSTR && FUSED), "instruction units run in the attention-only kernel");
   constexpr int RW = 16 * RB * NW, DPT = RG::BLOCKS / NW;
   constexpr int P0 = RG::NS - 1 < 3 ? RG::NS - 1 : 3;      // tiles issued before the queries are rotated
   const int lr = lane & 15, lg = lane >> 4;
@@ -279,16 +279,19 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   if (cglob >= (INSTR ? p.n_igroups : p.n_groups) * nch) return;
   const int grp = cglob / nch, chunk = cglob - grp * nch;
 
-  int b, g, qa, qb;
+  int b = 0, g, qa, qb;
   int ctx_len, slot_k;                             // key-range length; slot index of this chunk's states
   int64_t off;                                     // key-range start in the pool
+  int64_t pos_base = 0;                            // position of the first context token (fused step)
+  int pa = 0, pe = 0;                              // INSTR: the prompts behind the instruction
   if constexpr (INSTR) {
     int s = 0;
     bool ok;
     if (p.shared) {
       g = grp / p.S;
       s = grp - g * p.S;
-      const int pa = p.instr_start[s], pe = p.instr_start[s + 1];
+      pa = p.instr_start[s];
+      pe = p.instr_start[s + 1];
       // the instructions' prompt ranges must tile [0, B) so that every
       // question's instruction slots are written
       ok = pa >= 0 && pe >= pa && pe <= p.B && (s > 0 || pa == 0) && (s < p.S - 1 || pe == p.B);
@@ -302,6 +305,8 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
       b = find_prompt(p, qa, lane).b;
       ok = b < p.B;
       if (ok) s = instr_of_prompt(p.instr_start, p.S, b);
+      pa = b;
+      pe = b + 1;
     }
     off = ok ? p.instr_off[s] : 0;
     ctx_len = ok ? p.instr_len[s] : 0;
@@ -336,6 +341,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     ctx_len = p.ctx_len[b];
     off = p.ctx_off[b];
     slot_k = chunk;
+    if (FUSED && p.S > 0) pos_base = instr_pos_base(p.instr_start, p.instr_len, p.S, b);
   }
   const int G = p.G;
   const int nrows = (qb - qa) * G;
@@ -376,6 +382,22 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     qi[rb] = qa + rr / G;
     h[rb] = g * G + rr % G;
   }
+  // fused instruction unit: each row's query sits at instr_len + ctx_len[b] +
+  // seg_len of its own question, b being the prompt (among pa..pe-1) that holds it
+  int64_t row_base[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) row_base[rb] = static_cast<int64_t>(ctx_len) + pos_base;
+  if constexpr (INSTR && FUSED) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      int lo = pa, hi = pe - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (p.q_start[mid] <= qi[rb]) lo = mid; else hi = mid - 1;
+      }
+      row_base[rb] = static_cast<int64_t>(ctx_len) + p.ctx_len[lo];
+    }
+  }
   RL rl;
   issue_row_loads<T, D, FUSED, RB>(rl, p, qi, h, lg);
   TileOffsets<T, D, NW, NS> toff;
@@ -398,8 +420,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     const int s_raw = static_cast<int>(rl.s[rb]);
     act[rb] = in_range[rb] && rl.a[rb] != 0u && usable_seg_len(p, s_raw) >= 0;
     any_act = any_act || act[rb];
-    row_query<T, D, FUSED, RL::QN, (RL::TN > 0 ? RL::TN : 1)>(qf[rb], rl.q[rb], rl.th,
-                                                              static_cast<int64_t>(ctx_len) + s_raw);
+    row_query<T, D, FUSED, RL::QN, (RL::TN > 0 ? RL::TN : 1)>(qf[rb], rl.q[rb], rl.th, row_base[rb] + s_raw);
     if (!act[rb]) {
 #pragma unroll
       for (int ds = 0; ds < D / 32; ++ds) qf[rb][ds] = M::zero();
@@ -557,7 +578,8 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
       const int h = hq;
       float2* rot = reinterpret_cast<float2*>(qrows + L::QAREA);
       if (FUSED) {
-        const int64_t pos = static_cast<int64_t>(pi.len) + s;
+        const int64_t pos = static_cast<int64_t>(pi.len) + s +
+                            (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
         for (int jj = lane; jj < D / 2; jj += 64) {
           float cs, sn;
           rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
@@ -730,14 +752,9 @@ __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepPa
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int blk = static_cast<int>(blockIdx.x);
-  if (blk < p.ctx_blocks) {
-    context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
-  } else if constexpr (FUSED) {
-    segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks, wave, lane);
-  } else {
-    if (blk < p.ctx_blocks + p.instr_blocks) context_unit<T, D, NW, NS, false, RB, true>(p, sh.main, wave, lane);
-    else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks - p.instr_blocks, wave, lane);
-  }
+  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
+  else if (blk < p.ctx_blocks + p.instr_blocks) context_unit<T, D, NW, NS, FUSED, RB, true>(p, sh.main, wave, lane);
+  else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks - p.instr_blocks, wave, lane);
 }
 
 // ---------------------------------------------------------------------------

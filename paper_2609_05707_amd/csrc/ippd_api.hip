@@ -94,7 +94,15 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   // LDS serves both): 128 rows as 4 x 32, 256 as 8 x 32.
   const bool two_blocks_ok = bt->dtype == IPPD_DTYPE_BF16 && bt->head_dim == 128;
   int rows = bt->tile_rows;
-  if (rows == 0) rows = max_rows <= 16 ? 16 : (max_rows <= 32 ? 32 : (max_rows <= 64 ? 64 : (max_rows <= 128 || !two_blocks_ok ? 128 : 256)));
+  // a two-level batch's instruction rows (all questions behind it) favour at
+  // least 64-row units (measured against 32 at 6 contexts per instruction)
+  int64_t sized_rows = max_rows;
+  if (bt->num_instr > 0 && shared) {
+    const int64_t irows = static_cast<int64_t>(bt->max_instr_questions) * G;
+    const int64_t want = irows < 64 ? irows : 64;
+    if (want > sized_rows) sized_rows = want;
+  }
+  if (rows == 0) rows = sized_rows <= 16 ? 16 : (sized_rows <= 32 ? 32 : (sized_rows <= 64 ? 64 : (sized_rows <= 128 || !two_blocks_ok ? 128 : 256)));
   int rb = rows > 64 && two_blocks_ok ? 2 : 1;
   int waves = rows / (16 * rb);
   // fp32 at D = 128: the operands of eight waves do not fit their registers
@@ -177,15 +185,6 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   if (st != IPPD_OK) return st;
   if (!kv || !out || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt) return IPPD_ERR_NULL;
   if (fused ? (!q_new || !k_new || !v_new) : !q_rot_in) return IPPD_ERR_NULL;
-  if (fused && bt->num_instr > 0) {
-    // two-level batch: the instruction units take rotated queries, so the step
-    // runs as the append launch followed by the attention launches
-    if (!q_rot_out) return IPPD_ERR_NULL;
-    ippd_status_t a = ippd_append_kv(bt, q_new, k_new, v_new, q_rot_out, kv, stream);
-    if (a != IPPD_OK) return a;
-    return decode(bt, shared, false, nullptr, nullptr, nullptr, q_rot_out, nullptr, kv, out, lse, workspace,
-                  workspace_bytes, stream);
-  }
   if (!aligned16(out) || !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) ||
       !aligned16(kv->seg_vt) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3)))
     return IPPD_ERR_ALIGN;

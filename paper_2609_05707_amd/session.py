@@ -242,7 +242,7 @@ class DecodeBatch:
         q_rot = self.q_rot if q_rot is None else q_rot
         out = self.out if out is None else out
         lse = self.lse if lse is None else lse
-        qr = q_rot.data_ptr() if (write_q_rot or self.S) else None   # a two-level step needs q_rot
+        qr = q_rot.data_ptr() if write_q_rot else None
         lse_ptr = lse.data_ptr() if with_lse else None
         fn = L.standard_decode_step if standard else L.ippd_decode_step
         ws, wsb = (self.ws_std, self.ws_std_bytes) if standard else (self.ws_ippd, self.ws_ippd_bytes)

@@ -189,9 +189,6 @@ def test_instruction_level_validation(lib):
     assert lib.ippd_load_instructions(ctypes.byref(good), None, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_NULL
     assert lib.ippd_prefill_attention(ctypes.byref(good), 8, FAKE, FAKE, ctypes.byref(kv), FAKE, FAKE,
                                       None) == L.IPPD_ERR_SHAPE
-    # the fused step of a two-level batch needs q_rot (it runs the append first)
-    args = (ctypes.byref(good), FAKE, FAKE, FAKE, None, ctypes.byref(kv), FAKE, None, FAKE, 1 << 30, None)
-    assert lib.ippd_decode_step(*args) == L.IPPD_ERR_NULL
 
 
 def test_workspace_formula_with_instructions(lib):
