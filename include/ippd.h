@@ -237,6 +237,23 @@ ippd_status_t standard_decode_attention(const ippd_batch_t *batch, const void *q
                                         hipStream_t stream);
 
 /*
+ * Baseline: the dense-mask form of the same attention, the paper's own
+ * scheme (Sec. 4.1: the stacked prompt's new tokens attend over ALL its keys
+ * under the additive mask M_fin; Sec. 4.2).  The context part is computed as
+ * in ippd_decode_attention; the segment part attends every question's rows
+ * over the segments of ALL questions of the prompt and masks out the other
+ * questions' keys, so it forms and discards the cross-question scores the
+ * block-diagonal form never computes.  Same result, arguments and semantics
+ * as ippd_decode_attention (call after ippd_append_kv); one-level batches
+ * with max_questions <= 64 (else IPPD_ERR_SHAPE); workspace >=
+ * dense_decode_workspace_bytes(batch) (0: batch not supported).
+ */
+size_t dense_decode_workspace_bytes(const ippd_batch_t *batch);
+ippd_status_t dense_decode_attention(const ippd_batch_t *batch, const void *q_rot,
+                                     const ippd_kv_cache_t *kv, float *out, float *lse,
+                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Fused decode step: ippd_append_kv followed by ippd_decode_attention, in
  * the same two kernel launches as ippd_decode_attention.  q_new [Nt][Hq][D], k_new/v_new [Nt][Hkv][D] are the
  * raw (pre-rotation) projections of the token each active question feeds

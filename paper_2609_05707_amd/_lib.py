@@ -31,6 +31,7 @@ EXPORTED = [
     "ippd_load_context", "ippd_load_instructions", "ippd_load_segments", "ippd_append_kv",
     "ippd_decode_workspace_bytes", "standard_decode_workspace_bytes",
     "ippd_decode_attention", "standard_decode_attention",
+    "dense_decode_workspace_bytes", "dense_decode_attention",
     "ippd_decode_step", "standard_decode_step",
     "ippd_prefill_attention", "standard_prefill_attention",
     "ippd_status_string", "ippd_last_hip_error", "ippd_version",
@@ -101,10 +102,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ippd_load_segments.restype = st
     lib.ippd_append_kv.argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache), c_void_p]
     lib.ippd_append_kv.restype = st
-    for name in ("ippd_decode_workspace_bytes", "standard_decode_workspace_bytes"):
+    for name in ("ippd_decode_workspace_bytes", "standard_decode_workspace_bytes", "dense_decode_workspace_bytes"):
         getattr(lib, name).argtypes = [P(IppdBatch)]
         getattr(lib, name).restype = c_size_t
-    for name in ("ippd_decode_attention", "standard_decode_attention"):
+    for name in ("ippd_decode_attention", "standard_decode_attention", "dense_decode_attention"):
         getattr(lib, name).argtypes = [P(IppdBatch), c_void_p, P(IppdKvCache), c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]
         getattr(lib, name).restype = st
@@ -173,6 +174,16 @@ def standard_decode_attention(batch, q_rot, kv, out, lse, workspace, workspace_b
     _check("standard_decode_attention",
            load_library().standard_decode_attention(ctypes.byref(batch), q_rot, ctypes.byref(kv), out, lse,
                                                     workspace, workspace_bytes, stream))
+
+
+def dense_decode_workspace_bytes(batch) -> int:
+    return int(load_library().dense_decode_workspace_bytes(ctypes.byref(batch)))
+
+
+def dense_decode_attention(batch, q_rot, kv, out, lse, workspace, workspace_bytes, stream) -> None:
+    _check("dense_decode_attention",
+           load_library().dense_decode_attention(ctypes.byref(batch), q_rot, ctypes.byref(kv), out, lse, workspace,
+                                                 workspace_bytes, stream))
 
 
 def ippd_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, workspace, workspace_bytes,

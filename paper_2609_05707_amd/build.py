@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libippd.so")
 
-SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip", "prefill.hip"]
+SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip", "prefill.hip", "dense_mask.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -33,6 +33,7 @@ HIPCC_FLAGS = [
 SOURCE_FLAGS = {
     "decode_step.hip": ["-fno-honor-nans"],
     "prefill.hip": ["-fno-honor-nans"],
+    "dense_mask.hip": ["-fno-honor-nans"],
 }
 
 

@@ -907,6 +907,13 @@ static hipError_t launch_d(int waves, int rb, bool deep, int grid, const StepPar
   return hipGetLastError();
 }
 
+hipError_t launch_merge(const StepParams& p, hipStream_t s) {
+  if (p.Nt == 0) return hipSuccess;
+  if (p.D == 64) merge_kernel<64><<<static_cast<unsigned>(p.Nt) * p.merge_parts, kMergeThreads, 0, s>>>(p);
+  else merge_kernel<128><<<static_cast<unsigned>(p.Nt) * p.merge_parts, kMergeThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
 hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
   if (p.Nt == 0 || grid == 0) return hipSuccess;
   if (dtype == 0)

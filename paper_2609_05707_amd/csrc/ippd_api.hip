@@ -85,8 +85,10 @@ void fill_inv_freq(const ippd_batch_t* bt, double* out) {
 
 // Launch plan of a decode call.  Depends only on host fields, so the
 // workspace query and the launch agree.
-bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
+bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool dense = false) {
   if (check_batch(bt) != IPPD_OK) return false;
+  // dense-mask baseline: one-level batches, up to 64 questions per prompt
+  if (dense && (!shared || bt->num_instr > 0 || bt->max_questions > 64)) return false;
   const int G = bt->num_q_heads / bt->num_kv_heads;
   const int64_t max_rows = shared ? static_cast<int64_t>(bt->max_questions) * G : G;
   // rows per context unit: 16 * rb per wave.  bf16 at D = 128 with more than
@@ -141,7 +143,10 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   const int64_t state_bytes = static_cast<int64_t>(G) * (bt->head_dim + 4) * 4;
   int tpu = 1;
   while (tpu < waves && (seg_tasks + tpu - 1) / tpu > slots && 2 * tpu * state_bytes <= 32768) tpu *= 2;
-  const int64_t seg_blocks = (seg_tasks + tpu - 1) / tpu;
+  // dense-mask baseline: segment units are (prompt, kv head, row group)
+  const int64_t seg_blocks = dense ? n_groups * nrg : (seg_tasks + tpu - 1) / tpu;
+  // (its own kernel enumerates context units without the 8-slice padding)
+  const int64_t dense_grid = n_groups * max_chunks * nrg + n_groups * nrg;
   const int64_t grid = ctx_blocks + instr_blocks + seg_blocks;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) || n_igroups * max_ichunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
@@ -151,11 +156,12 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl) {
   pl->chunk = chunk;
   pl->max_chunks = static_cast<int>(max_chunks);
   pl->n_groups = static_cast<int>(n_groups);
-  pl->grid = static_cast<int>(grid);
+  pl->grid = static_cast<int>(dense ? dense_grid : grid);
   pl->ctx_blocks = static_cast<int>(ctx_blocks);
   pl->seg_blocks = static_cast<int>(seg_blocks);
   pl->seg_tpu = tpu;
   pl->deep = deep ? 1 : 0;
+  pl->dense = dense ? 1 : 0;
   pl->n_igroups = static_cast<int>(n_igroups);
   pl->nrg_i = nrg_i;
   pl->max_ichunks = static_cast<int>(max_ichunks);
@@ -180,7 +186,7 @@ ippd_status_t hip_status(hipError_t e) {
 ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void* q_new,
                      const void* k_new, const void* v_new, const void* q_rot_in, void* q_rot_out,
                      const ippd_kv_cache_t* kv, float* out, float* lse, void* workspace,
-                     size_t workspace_bytes, hipStream_t stream) {
+                     size_t workspace_bytes, hipStream_t stream, bool dense = false) {
   ippd_status_t st = check_batch(bt);
   if (st != IPPD_OK) return st;
   if (!kv || !out || !kv->ctx_k || !kv->ctx_vt || !kv->seg_k || !kv->seg_vt) return IPPD_ERR_NULL;
@@ -192,7 +198,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
             : !aligned16(q_rot_in))
     return IPPD_ERR_ALIGN;
   ippd::StepPlan pl;
-  if (!plan_step(bt, shared, &pl)) return IPPD_ERR_SHAPE;
+  if (!plan_step(bt, shared, &pl, dense)) return IPPD_ERR_SHAPE;
   if (bt->num_questions == 0) return IPPD_OK;
   if (!workspace || workspace_bytes < pl.workspace_bytes) return IPPD_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) & 255u) return IPPD_ERR_ALIGN;
@@ -232,6 +238,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
+  if (pl.dense) return hip_status(ippd::launch_dense(bt->dtype, pl.waves, pl.rb, pl.grid, p, stream));
   return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));
 }
 
@@ -396,6 +403,18 @@ ippd_status_t standard_decode_attention(const ippd_batch_t* bt, const void* q_ro
                                         hipStream_t stream) {
   return decode(bt, false, false, nullptr, nullptr, nullptr, q_rot, nullptr, kv, out, lse, workspace,
                 workspace_bytes, stream);
+}
+
+size_t dense_decode_workspace_bytes(const ippd_batch_t* bt) {
+  ippd::StepPlan pl;
+  return plan_step(bt, true, &pl, true) ? pl.workspace_bytes : 0;
+}
+
+ippd_status_t dense_decode_attention(const ippd_batch_t* bt, const void* q_rot, const ippd_kv_cache_t* kv,
+                                     float* out, float* lse, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  return decode(bt, true, false, nullptr, nullptr, nullptr, q_rot, nullptr, kv, out, lse, workspace,
+                workspace_bytes, stream, true);
 }
 
 ippd_status_t ippd_decode_step(const ippd_batch_t* bt, const void* q_new, const void* k_new,

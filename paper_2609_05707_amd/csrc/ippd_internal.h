@@ -61,6 +61,7 @@ struct StepPlan {
   int nrg_i;               // row groups per instruction group
   int max_ichunks;         // ceil(max_instr_len / chunk)
   int instr_blocks;        // instruction units, after the context units
+  int dense;               // dense-mask baseline: seg_blocks are dense segment units (prompt, kv head, row group)
   size_t part_slots;       // (max_chunks + 1 + max_ichunks) * Nt * Hq partial softmax states
                            // (context chunks, segment, instruction chunks)
   size_t off_acc, off_ml;  // byte offsets of the partial arrays in the workspace
@@ -123,6 +124,11 @@ hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
 hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s);
+// merge_kernel alone (the dense-mask baseline's second launch)
+hipError_t launch_merge(const StepParams& p, hipStream_t s);
+// dense-mask baseline: dense_kernel (context-chunk units, then dense segment
+// units) followed by merge_kernel
+hipError_t launch_dense(int dtype, int waves, int rb, int grid, const StepParams& p, hipStream_t s);
 // prefill_kernel for the batch dtype and head dimension (waves / rb fixed per
 // variant: see prefill_variant)
 hipError_t launch_prefill(int dtype, int head_dim, int grid, const PrefillParams& p, hipStream_t s);

@@ -124,6 +124,7 @@ class DecodeBatch:
             kv.seg_k = self.seg_k[layer].data_ptr()
             kv.seg_vt = self.seg_vt[layer].data_ptr()
             self.caches.append(kv)
+        self.ws_dense_bytes = L.dense_decode_workspace_bytes(self.batches[0])   # 0 if not supported
         self.ws_ippd_bytes = L.ippd_decode_workspace_bytes(self.batches[0])
         self.ws_std_bytes = L.standard_decode_workspace_bytes(self.batches[0])
         # the library needs no initialisation of its workspace (zeros for tidiness)
@@ -220,12 +221,21 @@ class DecodeBatch:
 
     def decode(self, layer: int, standard: bool = False, q_rot: Optional[torch.Tensor] = None,
                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-               with_lse: bool = True) -> None:
+               with_lse: bool = True, dense: bool = False) -> None:
+        """Attention after append: IPPD, the standard baseline or (dense=True) the
+        dense-mask baseline."""
         q_rot = self.q_rot if q_rot is None else q_rot
         out = self.out if out is None else out
         lse = self.lse if lse is None else lse
         lse_ptr = lse.data_ptr() if with_lse else None
-        if standard:
+        if dense:
+            if self.ws_dense_bytes == 0:
+                raise ValueError("the dense-mask baseline needs a one-level batch with <= 64 questions per prompt")
+            if getattr(self, "ws_dense", None) is None:
+                self.ws_dense = torch.zeros(self.ws_dense_bytes, dtype=torch.uint8, device=self.device)
+            L.dense_decode_attention(self.batches[layer], q_rot.data_ptr(), self.caches[layer], out.data_ptr(),
+                                     lse_ptr, self.ws_dense.data_ptr(), self.ws_dense_bytes, self.stream())
+        elif standard:
             L.standard_decode_attention(self.batches[layer], q_rot.data_ptr(), self.caches[layer],
                                         out.data_ptr(), lse_ptr, self.ws_std.data_ptr(),
                                         self.ws_std_bytes, self.stream())

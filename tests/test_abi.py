@@ -201,3 +201,17 @@ def test_workspace_formula_with_instructions(lib):
     want = r(slots * 64 * 4) + r(slots * 2 * 4)
     assert lib.ippd_decode_workspace_bytes(ctypes.byref(bt)) == want
     assert lib.standard_decode_workspace_bytes(ctypes.byref(bt)) == want
+
+
+def test_dense_baseline_validation(lib):
+    bt = valid_batch()
+    need = lib.dense_decode_workspace_bytes(ctypes.byref(bt))
+    assert need == lib.ippd_decode_workspace_bytes(ctypes.byref(bt))      # the same partial-state slots
+    assert decode_status(lib, bt, ws_bytes=need - 1, fn="dense_decode_attention") == L.IPPD_ERR_WORKSPACE
+    assert decode_status(lib, bt, q=None, fn="dense_decode_attention") == L.IPPD_ERR_NULL
+    many = valid_batch(max_questions=65)                                   # more than 64 questions per prompt
+    assert lib.dense_decode_workspace_bytes(ctypes.byref(many)) == 0
+    assert decode_status(lib, many, fn="dense_decode_attention") == L.IPPD_ERR_SHAPE
+    two = valid_batch(num_instr=1, max_instr_len=64, max_instr_questions=4, instr_start=FAKE, instr_off=FAKE,
+                      instr_len=FAKE)
+    assert decode_status(lib, two, fn="dense_decode_attention") == L.IPPD_ERR_SHAPE
