@@ -47,6 +47,7 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="emulated layers cycled per step")
     ap.add_argument("--no-standard", action="store_true", help="skip the standard baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense-mask baseline")
     ap.add_argument("--cpu-sample", type=int, default=400, help="question-steps the oracle computes")
     ap.add_argument("--chunk", type=int, default=0, help="context tokens per unit (0 = library default)")
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per context unit (0 = library default)")
@@ -90,6 +91,20 @@ def step_flops(st: W.Structure, t: int) -> int:
     for i in np.flatnonzero(act):
         b = st.prompt_of[i]
         tot += 4 * wl.hq * wl.head_dim * (int(st.ctx_len[b]) + int(seg[i]) + 1)
+    return tot
+
+
+def dense_flops(st: W.Structure, t: int) -> int:
+    """FLOPs of the dense-mask form: the context part as IPPD, the segment part
+    every active row of a prompt against the segments of all its questions."""
+    wl = st.wl
+    act = st.active(t)
+    seg = st.seg_len_at(t) + act                  # the step's token is appended first
+    tot = 0
+    for b in range(wl.num_prompts):
+        q0, q1 = st.q_start[b], st.q_start[b + 1]
+        n_act = int(act[q0:q1].sum())
+        tot += 4 * wl.hq * wl.head_dim * n_act * (int(st.ctx_len[b]) + int(seg[q0:q1].sum()))
     return tot
 
 
@@ -193,29 +208,29 @@ def main():
             db.seg_len[l].copy_(seg0)
         torch.cuda.synchronize()
 
-    def run(n_steps, standard=False, events=None, separate=False):
+    def run(n_steps, standard=False, events=None, separate=False, dense=False):
         for t in range(n_steps):
             d = t % data_steps
             set_step_active(d)
             for l in range(layers):
                 if events is not None:
                     events[t][l][0].record(stream)
-                if separate:
+                if separate or dense:
                     db.append(l, qs[d], ks[d], vs[d])
-                    db.decode(l, standard=standard)
+                    db.decode(l, standard=standard, dense=dense)
                 else:
                     db.decode_step(l, qs[d], ks[d], vs[d], standard=standard, write_q_rot=False)
                 if events is not None:
                     events[t][l][1].record(stream)
 
-    def timed(standard=False, separate=False):
+    def timed(standard=False, separate=False, dense=False):
         reset()
-        run(args.warmup, standard, separate=separate)
+        run(args.warmup, standard, separate=separate, dense=dense)
         reset()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        run(steps, standard, separate=separate)
+        run(steps, standard, separate=separate, dense=dense)
         e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / 1e3
@@ -246,11 +261,13 @@ def main():
     achieved = bytes_per_launch / k_avg / 1e9
     traffic = read_traffic(wl.wid)
     t_sep = timed(False, separate=True)
+    flags = {"ippd": err, "separate": db.err_flag()}
 
     def graph_time():
         """The same steps captured once into a HIP graph and replayed (kernels and
         arguments of the eager sequence; no host launch cost in the timed region)."""
         from paper_2609_05707_amd.driver import DecodeLoop
+        reset()                                   # the loop restores the lengths it starts from
         loop = DecodeLoop(db, [qs[t % data_steps] for t in range(steps)], [ks[t % data_steps] for t in range(steps)],
                           [vs[t % data_steps] for t in range(steps)], [acts[t % data_steps] for t in range(steps)])
         loop.capture()
@@ -271,6 +288,7 @@ def main():
         return best
 
     t_graph = graph_time()
+    flags["graph"] = db.err_flag()
 
     result = {
         "metric": METRIC,
@@ -314,6 +332,7 @@ def main():
     }
     if not args.no_standard:
         t_std = timed(True)
+        flags["standard"] = db.err_flag()
         std_b = [step_bytes(st, t % data_steps, standard=True) for t in range(steps)]
         ks_avg, _ = kernel_time(True)
         result["standard"] = {
@@ -324,6 +343,20 @@ def main():
             "avg_launch_us": round(ks_avg * 1e6, 3),
             "hbm_gbps_algorithmic": round(float(np.mean(std_b)) / ks_avg / 1e9, 1),
         }
+    if not args.no_dense and db.ws_dense_bytes > 0:
+        # the paper's own scheme (dense mask over the whole stacked prompt), as
+        # append + attention calls: compare with the IPPD separate calls
+        t_dense = timed(False, dense=True)
+        flags["dense"] = db.err_flag()
+        ippd_f = sum(step_flops(st, t % data_steps) for t in range(steps))
+        dense_f = sum(dense_flops(st, t % data_steps) for t in range(steps))
+        result["dense_mask"] = {
+            "us_per_layer_step": round(t_dense / (steps * layers) * 1e6, 3),
+            "vs_ippd_separate_calls": round(t_dense / t_sep, 3),
+            "flop_ratio": round(dense_f / ippd_f, 3),
+            "note": "append + dense_decode_attention (every row over all keys of its prompt, M_fin mask)",
+        }
+    result["err_flags"] = flags
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(st, kv0, args.cpu_sample)
     print(json.dumps(result), flush=True)

@@ -9,14 +9,18 @@
 //                        question of b x the G heads of g, keys = one context
 //                        chunk (every row sees all of them), as the split-K
 //                        context units of the IPPD path;
-//   dense segment units  (prompt b, kv head g, row group): the same rows, keys
-//                        = the segments of ALL questions of b in question
-//                        order; a segment tile is visible only to its own
-//                        question's rows, so the unit forms and discards the
+//   dense segment units  (prompt b, kv head g, segment chunk, row group): the
+//                        same rows, keys = one chunk of the segments of ALL
+//                        questions of b, concatenated in question order (in
+//                        32-token tiles, kDenseSegTiles tiles per chunk);
+//                        a segment tile is visible only to its own question's
+//                        rows, so the unit forms and discards the
 //                        cross-question scores that the per-question segment
 //                        units never compute.
-// Both write the partial states that merge_kernel folds (chunk slots, then the
-// segment slot), so the launch is followed by the IPPD merge.  Rows load their
+// Both write the partial states that merge_kernel folds: context chunk slots,
+// the segment slot (segment chunk 0, also the skip mark of a question not
+// served) and, for segment chunks 1.., the slots after it; so the launch is
+// followed by the IPPD merge.  Rows load their
 // rotated queries with ordinary loads consumed before the first tile DMA (no
 // loads in flight across the ring's counted waits).  A prompt holds at most
 // 64 questions: lane l of every wave keeps the length of question l.
@@ -56,18 +60,16 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
   const int lr = lane & 15, lg = lane >> 4;
   const int blk = static_cast<int>(blockIdx.x);
   const int nctx = p.n_groups * p.max_chunks * p.nrg;
+  const int nseg = p.max_ichunks + 1;             // segment chunks per group
   const bool seg = blk >= nctx;
-  int grp, chunk, rg;
-  if (!seg) {
-    const int cg = blk / p.nrg;
-    rg = blk - cg * p.nrg;
-    grp = cg / p.max_chunks;
-    chunk = cg - grp * p.max_chunks;
-  } else {
-    const int u = blk - nctx;
-    grp = u / p.nrg;
-    rg = u - grp * p.nrg;
-    chunk = 0;
+  int grp, chunk, rg;                             // chunk: context chunk, or segment chunk
+  {
+    const int u = seg ? blk - nctx : blk;
+    const int nch = seg ? nseg : p.max_chunks;
+    const int cg = u / p.nrg;
+    rg = u - cg * p.nrg;
+    grp = cg / nch;
+    chunk = cg - grp * nch;
   }
   if (grp >= p.n_groups) return;
   const int g = grp / p.B, b = grp - g * p.B;
@@ -114,7 +116,7 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
     const T* src = static_cast<const T*>(p.q_rot_in) + (static_cast<int64_t>(qi[rb]) * p.Hq + h[rb]) * D + 8 * lg;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = M::load(src + 32 * ds);
-    if (seg && in_range && !act[rb] && lg == 0) {   // not served: the merge skips the question
+    if (seg && chunk == 0 && in_range && !act[rb] && lg == 0) {   // not served: the merge skips the question
       const int64_t slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + qi[rb]) * p.Hq + h[rb];
       *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, -1.f);
     }
@@ -124,17 +126,42 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
   for (int rb = 0; rb < RB; ++rb) any = any || act[rb];
   if (!__syncthreads_or(any)) return;
 
-  // key tiles: one context chunk, or the segments of every question in order
+  // key tiles: one context chunk, or one chunk of the concatenated segment tiles
   const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
   const int64_t k1 = min(k0 + p.chunk, off + static_cast<int64_t>(ctx_len));
-  int ntiles;
+  int ntiles, j0 = 0, tt0 = 0;
   if (!seg) {
     ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
   } else {
-    ntiles = 0;
-    for (int j = 0; j < nq; ++j) ntiles += (__builtin_amdgcn_readlane(len_v, j) + 31) >> 5;
+    // tiles per question (lane l: question l), their inclusive prefix over the lanes
+    const int nt_v = (len_v + 31) >> 5;
+    int incl = nt_v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int y = __shfl_up(incl, d, 64);
+      incl += lane >= d ? y : 0;
+    }
+    const int total = __builtin_amdgcn_readlane(incl, 63);
+    const int tpc = kDenseSegTiles;
+    const int first = chunk * tpc;
+    ntiles = max(0, min(first + tpc, total) - first);
+    // the chunk starts in question j0 (the first whose tiles reach past `first`), tile tt0 of it
+    j0 = __popcll(__ballot(lane < nq && incl <= first));
+    tt0 = j0 < nq ? first - (__builtin_amdgcn_readlane(incl, j0) - __builtin_amdgcn_readlane(nt_v, j0)) : 0;
   }
   ntiles = __builtin_amdgcn_readfirstlane(ntiles);
+  const int slot_k = !seg ? chunk : (chunk == 0 ? p.max_chunks : p.max_chunks + chunk);
+  if (ntiles == 0) {
+    // a segment chunk past the prompt's tiles: an empty state for every served row
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      if (act[rb] && lg == 0) {
+        const int64_t slot = (static_cast<int64_t>(slot_k) * p.Nt + qi[rb]) * p.Hq + h[rb];
+        *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, 0.f);
+      }
+    }
+    return;
+  }
   const T* kctx = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
   const T* vctx = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
   const T* kseg = static_cast<const T*>(p.seg_k) + (static_cast<int64_t>(qa) * p.Hkv + g) * p.seg_cap * D;
@@ -145,7 +172,7 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
   toff.init(wave, lane);
 
   wait_vmcnt<0>();                                // only tile DMAs are counted from here
-  int ti_idx = 0, ji = dense_next_question(len_v, nq, 0), ti = 0;   // issue cursor
+  int ti_idx = 0, ji = j0, ti = tt0;              // issue cursor
   const int last = ntiles - 1;
 #pragma unroll
   for (int st = 0; st < RG::NS - 1; ++st) {
@@ -168,7 +195,7 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
   wait_tiles<DPT, RG::NS - 2>(min(last, RG::NS - 2));
   __syncthreads();
   qk_tile<T, D, NS, RB>(ring, qf, sc, lr, lg);
-  int jc = dense_next_question(len_v, nq, 0), tc = 0;   // compute cursor (segment units)
+  int jc = j0, tc = tt0;                          // compute cursor (segment units)
   for (int t = 0; t < ntiles; ++t) {
     if (t < last) {
       wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
@@ -213,7 +240,6 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
   }
   wait_vmcnt<0>();                                // no LDS-DMA may outlive the workgroup
 
-  const int slot_k = seg ? p.max_chunks : chunk;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     if (!act[rb]) continue;

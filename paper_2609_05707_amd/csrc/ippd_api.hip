@@ -143,10 +143,14 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   const int64_t state_bytes = static_cast<int64_t>(G) * (bt->head_dim + 4) * 4;
   int tpu = 1;
   while (tpu < waves && (seg_tasks + tpu - 1) / tpu > slots && 2 * tpu * state_bytes <= 32768) tpu *= 2;
-  // dense-mask baseline: segment units are (prompt, kv head, row group)
-  const int64_t seg_blocks = dense ? n_groups * nrg : (seg_tasks + tpu - 1) / tpu;
-  // (its own kernel enumerates context units without the 8-slice padding)
-  const int64_t dense_grid = n_groups * max_chunks * nrg + n_groups * nrg;
+  // dense-mask baseline: segment units (prompt, kv head, segment chunk, row
+  // group) split the prompt's concatenated segment tiles into chunks of
+  // kDenseSegTiles tiles; chunk 0 writes the segment slot, chunks 1.. the
+  // slots after it (where a two-level batch keeps its instruction chunks)
+  const int64_t seg_tiles = static_cast<int64_t>(bt->max_questions) * ((bt->seg_capacity + 31) / 32);
+  const int64_t seg_chunks = dense ? (seg_tiles + ippd::kDenseSegTiles - 1) / ippd::kDenseSegTiles : 0;
+  const int64_t seg_blocks = dense ? n_groups * seg_chunks * nrg : (seg_tasks + tpu - 1) / tpu;
+  const int64_t dense_grid = n_groups * max_chunks * nrg + seg_blocks;
   const int64_t grid = ctx_blocks + instr_blocks + seg_blocks;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) || n_igroups * max_ichunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
@@ -164,9 +168,9 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   pl->dense = dense ? 1 : 0;
   pl->n_igroups = static_cast<int>(n_igroups);
   pl->nrg_i = nrg_i;
-  pl->max_ichunks = static_cast<int>(max_ichunks);
+  pl->max_ichunks = static_cast<int>(dense ? seg_chunks - 1 : max_ichunks);
   pl->instr_blocks = static_cast<int>(instr_blocks);
-  pl->part_slots = static_cast<size_t>(max_chunks + 1 + max_ichunks) * bt->num_questions * bt->num_q_heads;
+  pl->part_slots = static_cast<size_t>(max_chunks + 1 + pl->max_ichunks) * bt->num_questions * bt->num_q_heads;
   pl->off_acc = 0;
   pl->off_ml = pl->off_acc + round256(pl->part_slots * bt->head_dim * sizeof(float));
   pl->workspace_bytes = pl->off_ml + round256(pl->part_slots * 2 * sizeof(float));

@@ -10,6 +10,7 @@ namespace ippd {
 constexpr int kMaxQuestionsPerPrompt = 1024;   // LDS list of a prompt's active questions
 constexpr int kMaxGroup = 16;                  // query heads per kv head (one MFMA row block)
 constexpr int kMaxHalfDim = 64;                // D/2 for D <= 128
+constexpr int kDenseSegTiles = 8;              // dense-mask baseline: 32-token tiles per segment chunk
 
 struct LoadContextParams {
   const void* k_raw; const void* v_raw;     // [pool][Hkv][D]

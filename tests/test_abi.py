@@ -206,7 +206,7 @@ def test_workspace_formula_with_instructions(lib):
 def test_dense_baseline_validation(lib):
     bt = valid_batch()
     need = lib.dense_decode_workspace_bytes(ctypes.byref(bt))
-    assert need == lib.ippd_decode_workspace_bytes(ctypes.byref(bt))      # the same partial-state slots
+    assert need >= lib.ippd_decode_workspace_bytes(ctypes.byref(bt))      # + any segment chunk slots
     assert decode_status(lib, bt, ws_bytes=need - 1, fn="dense_decode_attention") == L.IPPD_ERR_WORKSPACE
     assert decode_status(lib, bt, q=None, fn="dense_decode_attention") == L.IPPD_ERR_NULL
     many = valid_batch(max_questions=65)                                   # more than 64 questions per prompt
