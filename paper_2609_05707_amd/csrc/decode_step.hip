@@ -771,7 +771,6 @@ __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepPa
 // metadata; only part 0 of a question reads its segment length, and
 // advances it in the fused step.
 // ---------------------------------------------------------------------------
-constexpr int kMergeThreads = 512;
 constexpr int kMergeBatch = 8;       // partial states in flight per thread
 
 // Exact combination of partial softmax states (m, l, a) in 2^(c*x) units;

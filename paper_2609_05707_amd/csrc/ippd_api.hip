@@ -230,12 +230,12 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.S = bt->num_instr; p.max_instr_len = bt->max_instr_len; p.max_instr_questions = bt->max_instr_questions;
   p.n_igroups = pl.n_igroups; p.nrg_i = pl.nrg_i; p.max_ichunks = pl.max_ichunks; p.instr_blocks = pl.instr_blocks;
   // merge: enough threads per item that each folds at most 8 of the
-  // max_chunks + 1 partial states; items split over workgroups of 512
+  // max_chunks + 1 partial states; items split over workgroups of kMergeThreads
   {
     int ph = 1;
     while (ph < 8 && (pl.max_chunks + 1 + pl.max_ichunks + ph - 1) / ph > 8) ph *= 2;
     const int items = bt->num_q_heads * (bt->head_dim / 8);
-    const int per = 512 / ph;
+    const int per = ippd::kMergeThreads / ph;
     p.merge_phases = ph;
     p.merge_parts = (items + per - 1) / per;
   }

@@ -11,6 +11,11 @@ constexpr int kMaxQuestionsPerPrompt = 1024;   // LDS list of a prompt's active 
 constexpr int kMaxGroup = 16;                  // query heads per kv head (one MFMA row block)
 constexpr int kMaxHalfDim = 64;                // D/2 for D <= 128
 constexpr int kDenseSegTiles = 8;              // dense-mask baseline: 32-token tiles per segment chunk
+#ifndef IPPD_MERGE_THREADS
+#define IPPD_MERGE_THREADS 256
+#endif
+constexpr int kMergeThreads = IPPD_MERGE_THREADS;   // merge_kernel workgroup size (256 measured ahead of 512
+                                                    // when a call has few questions, equal otherwise)
 
 struct LoadContextParams {
   const void* k_raw; const void* v_raw;     // [pool][Hkv][D]
