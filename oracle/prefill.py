@@ -36,17 +36,20 @@ from . import ippd as O
 
 
 def standard_prefill_question(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base: float,
-                              scale: Optional[float] = None, rows: Optional[Sequence[int]] = None):
-    """Path 1 for one question: causal attention over [context; question].
+                              scale: Optional[float] = None, rows: Optional[Sequence[int]] = None,
+                              instr=None):
+    """Path 1 for one question: causal attention over [instruction; context; question].
 
     ctx_* are raw [Lc, H, D] (keys/values with Hkv heads, queries with Hq);
-    seg_* the question's raw tokens [s, H, D].  ``rows`` selects sequence
-    positions to compute (default all n = Lc + s).  Returns out [n, Hq, D]
-    (NaN for rows not computed).
+    seg_* the question's raw tokens [s, H, D]; ``instr`` optionally
+    (k, v, q) of an instruction p placed before the context (Sec. 4.1: p at
+    [0, |p|)).  ``rows`` selects sequence positions to compute (default all
+    n = |p| + Lc + s).  Returns out [n, Hq, D] (NaN for rows not computed).
     """
-    K = np.concatenate([np.asarray(ctx_k, np.float64), np.asarray(seg_k, np.float64)], axis=0)
-    V = np.concatenate([np.asarray(ctx_v, np.float64), np.asarray(seg_v, np.float64)], axis=0)
-    Q = np.concatenate([np.asarray(ctx_q, np.float64), np.asarray(seg_q, np.float64)], axis=0)
+    parts = ([instr] if instr is not None else []) + [(ctx_k, ctx_v, ctx_q), (seg_k, seg_v, seg_q)]
+    K = np.concatenate([np.asarray(x[0], np.float64) for x in parts], axis=0)
+    V = np.concatenate([np.asarray(x[1], np.float64) for x in parts], axis=0)
+    Q = np.concatenate([np.asarray(x[2], np.float64) for x in parts], axis=0)
     n, hkv, d = K.shape
     hq = Q.shape[1]
     G = hq // hkv
@@ -64,13 +67,19 @@ def standard_prefill_question(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base: fl
 
 
 def prefill_standard(ctx_k, ctx_v, ctx_q, ctx_start, q_start, seg_k, seg_v, seg_q, seg_start,
-                     base: float, scale: Optional[float] = None, ctx_rows=None, seg_rows=None):
+                     base: float, scale: Optional[float] = None, ctx_rows=None, seg_rows=None,
+                     instr=None):
     """Path 1 over a ragged batch of prompts.
 
     Packed inputs as in the decode oracle: prompt b's context tokens at
     ctx_start[b]:ctx_start[b+1], question i's tokens at seg_start[i]:seg_start[i+1].
+    ``instr`` (two-level batch) is (prompt_start, tok_start, k, v, q): prompts
+    prompt_start[s]:prompt_start[s+1] sit behind instruction s, whose raw
+    tokens are k/v/q[tok_start[s]:tok_start[s+1]]; every question's own
+    prompt is then [p_s; c_b; x_i].
     ``ctx_rows`` / ``seg_rows`` optionally list packed token indices to compute.
-    Returns out_ctx [sum Lc, Hq, D] and out_seg [sum s, Hq, D] (NaN where not computed).
+    Returns out_ctx [sum Lc, Hq, D] and out_seg [sum s, Hq, D] (NaN where not
+    computed), and with ``instr`` also out_instr [sum |p|, Hq, D].
     """
     hq, d = ctx_q.shape[1], ctx_q.shape[2]
     B = len(ctx_start) - 1
@@ -78,32 +87,57 @@ def prefill_standard(ctx_k, ctx_v, ctx_q, ctx_start, q_start, seg_k, seg_v, seg_
     out_seg = np.full((int(seg_start[-1]), hq, d), np.nan)
     want_c = None if ctx_rows is None else set(int(x) for x in ctx_rows)
     want_s = None if seg_rows is None else set(int(x) for x in seg_rows)
+    ins_of = (lambda b: None)
+    out_ins = None
+    if instr is not None:
+        pstart, tstart, ik, iv, iq = instr
+        out_ins = np.full((int(tstart[-1]), hq, d), np.nan)
+
+        def ins_of(b):
+            s_ = int(np.searchsorted(pstart, b, side="right") - 1)
+            t0, t1 = int(tstart[s_]), int(tstart[s_ + 1])
+            return s_, (ik[t0:t1], iv[t0:t1], iq[t0:t1])
+        # instruction rows: causal over the instruction alone
+        for s_ in range(len(tstart) - 1):
+            t0, t1 = int(tstart[s_]), int(tstart[s_ + 1])
+            if t1 > t0:
+                e = ik[t0:t0]
+                o = standard_prefill_question(ik[t0:t1], iv[t0:t1], iq[t0:t1], e, e, iq[t0:t0], base, scale)
+                out_ins[t0:t1] = o
     for b in range(B):
         c0, c1 = int(ctx_start[b]), int(ctx_start[b + 1])
         lc = c1 - c0
+        ins = ins_of(b)
+        pre = None if ins is None else ins[1]
+        lp = 0 if pre is None else len(pre[0])
         qs = range(int(q_start[b]), int(q_start[b + 1]))
-        # context rows: causal over the context alone (the same in every question's prompt)
-        rows = [t for t in range(lc) if want_c is None or c0 + t in want_c]
+        # context rows: causal over [instruction; context] (the same in every question's prompt)
+        rows = [lp + t for t in range(lc) if want_c is None or c0 + t in want_c]
         if rows:
             o = standard_prefill_question(ctx_k[c0:c1], ctx_v[c0:c1], ctx_q[c0:c1],
-                                          ctx_k[c0:c0], ctx_v[c0:c0], ctx_q[c0:c0], base, scale, rows)
-            out_ctx[c0 + np.asarray(rows)] = o[rows]
+                                          ctx_k[c0:c0], ctx_v[c0:c0], ctx_q[c0:c0], base, scale, rows, pre)
+            out_ctx[c0 + np.asarray(rows) - lp] = o[rows]
         for i in qs:
             s0, s1 = int(seg_start[i]), int(seg_start[i + 1])
-            rows = [lc + u for u in range(s1 - s0) if want_s is None or s0 + u in want_s]
+            rows = [lp + lc + u for u in range(s1 - s0) if want_s is None or s0 + u in want_s]
             if not rows:
                 continue
             o = standard_prefill_question(ctx_k[c0:c1], ctx_v[c0:c1], ctx_q[c0:c1],
-                                          seg_k[s0:s1], seg_v[s0:s1], seg_q[s0:s1], base, scale, rows)
-            out_seg[s0 + np.asarray(rows) - lc] = o[rows]
+                                          seg_k[s0:s1], seg_v[s0:s1], seg_q[s0:s1], base, scale, rows, pre)
+            out_seg[s0 + np.asarray(rows) - lp - lc] = o[rows]
+    if instr is not None:
+        return out_ctx, out_seg, out_ins
     return out_ctx, out_seg
 
 
 def stacked_prefill(ctx_k, ctx_v, ctx_q, ctx_start, q_start, seg_k, seg_v, seg_q, seg_start,
-                    base: float, scale: Optional[float] = None):
+                    base: float, scale: Optional[float] = None, instr=None):
     """Path 2: every header row of the literal stacked prompt under M_fin.
 
-    Returns out_ctx [sum Lc, Hq, D] and out_seg [sum s, Hq, D].
+    ``instr`` optionally (k, v, q) of one instruction p shared by all the
+    contexts of this stacked prompt (ctx = 0 tokens at [0, |p|), Sec. 4.1).
+    Returns out_ctx [sum Lc, Hq, D] and out_seg [sum s, Hq, D] (and out_instr
+    [|p|, Hq, D] with ``instr``).
     """
     hkv, d = ctx_k.shape[1], ctx_k.shape[2]
     hq = ctx_q.shape[1]
@@ -115,14 +149,18 @@ def stacked_prefill(ctx_k, ctx_v, ctx_q, ctx_start, q_start, seg_k, seg_v, seg_q
     ctx_len = [int(ctx_start[b + 1] - ctx_start[b]) for b in range(B)]
     qlen = [int(seg_start[i + 1] - seg_start[i]) for i in range(nt)]
     # no answer token exists yet: every question's slot in the step round is a pad
-    meta = O.build_stacked_metadata(0, ctx_len, list(q_start), qlen, [0] * nt, [False] * nt)
+    lp = 0 if instr is None else len(instr[0])
+    meta = O.build_stacked_metadata(lp, ctx_len, list(q_start), qlen, [0] * nt, [False] * nt)
     n = len(meta.src)
     K = np.zeros((n, hkv, d))
     V = np.zeros((n, hkv, d))
     Q = np.zeros((n, hq, d))
     header = []
     for t, (kind, owner, idx) in enumerate(meta.src):
-        if kind == "ctx":
+        if kind == "instr":
+            K[t], V[t], Q[t] = instr[0][idx], instr[1][idx], instr[2][idx]
+            header.append((t, "instr", idx))
+        elif kind == "ctx":
             j = int(ctx_start[owner]) + idx
             K[t], V[t], Q[t] = ctx_k[j], ctx_v[j], ctx_q[j]
             header.append((t, "ctx", j))
@@ -136,9 +174,12 @@ def stacked_prefill(ctx_k, ctx_v, ctx_q, ctx_start, q_start, seg_k, seg_v, seg_q
     add_mask = np.where(O.mask_predicates(meta, rows), 0.0, -np.inf)
     out_ctx = np.full((int(ctx_start[-1]), hq, d), np.nan)
     out_seg = np.full((int(seg_start[-1]), hq, d), np.nan)
+    out_ins = np.full((lp, hq, d), np.nan)
     for r, (t, kind, j) in enumerate(header):
         qr = O.rope(Q[t], meta.pos[t], base)
-        dst = out_ctx if kind == "ctx" else out_seg
+        dst = {"ctx": out_ctx, "seg": out_seg, "instr": out_ins}[kind]
         for h in range(hq):
             dst[j, h], _ = O.attend(qr[h], Kr[h // G], V[:, h // G, :], scale, add_mask[r])
+    if instr is not None:
+        return out_ctx, out_seg, out_ins
     return out_ctx, out_seg

@@ -82,6 +82,47 @@ def test_stacked_prompt_equals_standard_prompting(seed):
     np.testing.assert_allclose(a[1], b[1], atol=1e-12)
 
 
+@pytest.mark.parametrize("seed", [7, 8])
+def test_two_level_prefill_equals_stacked_prompt(seed):
+    """Two-level prefill (Sec. 4.4): one instruction shared by every context of the
+    stacked prompt.  Per-question standard prompting [p; c_b; x_i] equals the
+    literal stacked header under M_fin, instruction rows included."""
+    c = _case(seed, [6, 9, 4], [2, 1, 3])
+    r = np.random.default_rng(seed + 50)
+    lp = 5
+    ik, iv = r.standard_normal((2, lp, 2, 32))
+    iq = r.standard_normal((lp, 8, 32))
+    a = P.prefill_standard(c["ck"], c["cv"], c["cq"], c["ctx_start"], c["q_start"], c["sk"], c["sv"], c["sq"],
+                           c["seg_start"], 10000.0, instr=(np.array([0, 3]), np.array([0, lp]), ik, iv, iq))
+    b = P.stacked_prefill(c["ck"], c["cv"], c["cq"], c["ctx_start"], c["q_start"], c["sk"], c["sv"], c["sq"],
+                          c["seg_start"], 10000.0, instr=(ik, iv, iq))
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, atol=1e-12)
+
+
+def test_two_level_prefill_rows_are_causal_attention_sdpa():
+    """One question's prompt [p; c; x]: every row is causal attention at real
+    positions (torch SDPA in fp64, keys and queries rotated by the complex form)."""
+    c = _case(9, [7], [1], qlen=(4, 4))
+    r = np.random.default_rng(60)
+    lp = 6
+    ik, iv = r.standard_normal((2, lp, 2, 32))
+    iq = r.standard_normal((lp, 8, 32))
+    oc, os_, oi = P.prefill_standard(c["ck"], c["cv"], c["cq"], c["ctx_start"], c["q_start"], c["sk"], c["sv"],
+                                     c["sq"], c["seg_start"], 10000.0,
+                                     instr=(np.array([0, 1]), np.array([0, lp]), ik, iv, iq))
+    K = np.concatenate([ik, c["ck"], c["sk"]])
+    V = np.concatenate([iv, c["cv"], c["sv"]])
+    Q = np.concatenate([iq, c["cq"], c["sq"]])
+    n = len(K)
+    Kr = np.stack([rope_complex(K[t], t, 10000.0) for t in range(n)])
+    Qr = np.stack([rope_complex(Q[t], t, 10000.0) for t in range(n)])
+    qt, kt, vt = (torch.from_numpy(a).permute(1, 0, 2)[None] for a in (Qr, Kr, V))
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True, enable_gqa=True)
+    ref = ref[0].permute(1, 0, 2).numpy()
+    np.testing.assert_allclose(np.concatenate([oi, oc, os_]), ref, atol=1e-12)
+
+
 def test_context_rows_ignore_the_questions_and_rows_are_prefix_closed():
     """Causality: a context row does not change when questions (or later context
     tokens) are appended; it equals the same row of a prefill of the prefix alone."""
@@ -128,16 +169,27 @@ def test_planted_mistakes_are_caught(monkeypatch):
     good_spq = P.standard_prefill_question
 
     # 1. causal window one key short (a row not seeing itself)
-    def short(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale=None, rows=None):
-        out = good_spq(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale, rows)
-        K = np.concatenate([ctx_k, seg_k])
-        for t in (range(len(K)) if rows is None else rows):
+    def short(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale=None, rows=None, instr=None):
+        out = good_spq(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale, rows, instr)
+        n = len(ctx_k) + len(seg_k) + (0 if instr is None else len(instr[0]))
+        for t in (range(n) if rows is None else rows):
             if t > 0:
-                o = good_spq(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale, [t - 1])
+                o = good_spq(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale, [t - 1], instr)
                 out[t] = o[t - 1]
         return out
     monkeypatch.setattr(P, "standard_prefill_question", short)
     assert not _passes(test_prefill_rows_are_causal_attention_sdpa)
+    assert not _passes(test_two_level_prefill_rows_are_causal_attention_sdpa)
+    monkeypatch.setattr(P, "standard_prefill_question", good_spq)
+
+    # 1b. the instruction dropped from the context and question rows' prompts
+    def no_instr(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale=None, rows=None, instr=None):
+        lp = 0 if instr is None else len(instr[0])
+        o = good_spq(ctx_k, ctx_v, ctx_q, seg_k, seg_v, seg_q, base, scale,
+                     None if rows is None else [t - lp for t in rows])
+        return np.concatenate([np.full((lp,) + o.shape[1:], np.nan), o])
+    monkeypatch.setattr(P, "standard_prefill_question", no_instr)
+    assert not _passes(test_two_level_prefill_rows_are_causal_attention_sdpa)
     monkeypatch.setattr(P, "standard_prefill_question", good_spq)
 
     # 2. question tokens placed one position late (positions Lc+1 ..)
