@@ -2,7 +2,7 @@
 """Benchmark of the stacked-prompt prefill attention on one MI355X.
 
 For each workload, one prefill call computes the attention output of every
-header token (every context token and every question token of every
+header token (every instruction, context and question token of every
 prompt) for one layer; ippd_prefill_attention serves all question tokens of
 a prompt from one pass over its context and computes the context rows once,
 standard_prefill_attention prefills each question's own prompt
@@ -51,31 +51,45 @@ WORKLOADS = {
     # 8 ragged prompts: context U{1024..8192}, 4..32 questions of U{8..32} tokens.
     "ragged-b8": dict(wid=502, num_prompts=8, ctx_len=(1024, 8192), questions=(4, 32), question_tokens=0,
                       seg_len=(8, 32)),
+    # two-level (Sec. 4.4): 8 contexts of 1024 tokens behind 2 instructions of
+    # 2048 tokens (4 contexts each), 8 questions of 16 tokens per context.
+    "two-level-b8-cpi4-lp2048": dict(wid=503, num_prompts=8, ctx_len=(1024, 1024), questions=(8, 8),
+                                     question_tokens=16, seg_len=(0, 0), instr=(4, (2048, 2048))),
 }
 
 
 def make(name: str) -> W.DecodeWorkload:
-    return W.custom_workload(name=name, dtype="bf16", hq=32, hkv=8, head_dim=128, steps=1, value_std=0.5,
-                             **WORKLOADS[name])
+    kw = {k: v for k, v in WORKLOADS[name].items() if k != "instr"}
+    return W.custom_workload(name=name, dtype="bf16", hq=32, hkv=8, head_dim=128, steps=1, value_std=0.5, **kw)
 
 
-def flops(st: W.Structure, standard: bool) -> float:
-    """Algorithmic FLOPs of one call: 4*D*Hq per visible (query row, key) pair."""
+def flops(st: W.Structure, standard: bool, ins=None) -> float:
+    """Algorithmic FLOPs of one call: 4*D*Hq per visible (query row, key) pair.
+    The baseline computes the rows of an instruction and of a context once per
+    question whose prompt holds them, IPPD once."""
     wl = st.wl
     per = 4.0 * wl.head_dim * wl.hq
     tot = 0.0
+    s_of = (np.searchsorted(ins.prompt_start, np.arange(wl.num_prompts), side="right") - 1
+            if ins is not None else None)
+    if ins is not None:
+        for s_ in range(len(ins.lp)):
+            lp = int(ins.lp[s_])
+            nq = int(st.q_start[ins.prompt_start[s_ + 1]] - st.q_start[ins.prompt_start[s_]])
+            tot += per * lp * (lp + 1) / 2 * (nq if standard else 1)
     for b in range(wl.num_prompts):
         lc = int(st.ctx_len[b])
+        lp = int(ins.lp[s_of[b]]) if ins is not None else 0
         qs = range(int(st.q_start[b]), int(st.q_start[b + 1]))
-        ctx_pairs = lc * (lc + 1) / 2
+        ctx_pairs = lc * lp + lc * (lc + 1) / 2
         tot += per * ctx_pairs * (len(qs) if standard else 1)   # context rows: once per question / once
         for i in qs:
             s = int(st.seg_len0[i])
-            tot += per * (s * lc + s * (s + 1) / 2)
+            tot += per * (s * (lp + lc) + s * (s + 1) / 2)
     return tot
 
 
-def cpu_baseline(st, kv, pq, budget_rows: int):
+def cpu_baseline(st, kv, pq, budget_rows: int, ins=None, iq=None):
     """The fp64 oracle on the first question rows and evenly spaced context rows."""
     from oracle import prefill as P
     try:
@@ -86,9 +100,11 @@ def cpu_baseline(st, kv, pq, budget_rows: int):
     nc = int(st.ctx_start[-1])
     ctx_rows = np.linspace(0, nc - 1, num=budget_rows // 2).astype(int).tolist()
     seg_rows = list(range(min(budget_rows // 2, int(st.seg_start[-1]))))
+    # (a two-level batch also recomputes its instruction rows: they are not counted)
+    instr = None if ins is None else (ins.prompt_start, ins.tok_start, ins.k, ins.v, iq)
     t0 = time.perf_counter()
     P.prefill_standard(kv.ctx_k, kv.ctx_v, pq.ctx_q, st.ctx_start, st.q_start, kv.seg_k, kv.seg_v, pq.seg_q,
-                       st.seg_start, st.wl.rope_base, ctx_rows=ctx_rows, seg_rows=seg_rows)
+                       st.seg_start, st.wl.rope_base, ctx_rows=ctx_rows, seg_rows=seg_rows, instr=instr)
     dt = time.perf_counter() - t0
     n = len(ctx_rows) + len(seg_rows)
     return {"value": n / dt, "unit": "header tokens/s", "cores": int(threads), "kind": "oracle",
@@ -105,11 +121,20 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
     kv = W.layer_kv(st)
     pq = W.prefill_queries(st)
     cap = max(8, int(st.seg_len0.max()))
+    ins = iq = None
+    extra = {}
+    if "instr" in WORKLOADS[name]:
+        cpi, lp = WORKLOADS[name]["instr"]
+        ins = W.instructions(st, cpi, lp)
+        iq = W.instruction_queries(st, ins)
+        extra = dict(instr_len=ins.lp.tolist(), instr_prompt_start=ins.prompt_start.tolist())
     db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
-                     rope_base=wl.rope_base)
+                     rope_base=wl.rope_base, **extra)
+    if ins is not None:
+        db.load_instructions(0, ins.k, ins.v)
     db.load_context(0, kv.ctx_k, kv.ctx_v)
     db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
-    q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0)
+    q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0, instr_q=iq)
     oc, os_ = db.prefill_outputs()
     bound = max(int(st.seg_len0[st.q_start[b]:st.q_start[b + 1]].sum()) for b in range(wl.num_prompts))
     stream = torch.cuda.current_stream()
@@ -129,8 +154,8 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
     t_ippd = timed(False)
     t_std = timed(True)
     assert db.err_flag() == 0
-    tokens = int(st.ctx_start[-1] + st.seg_start[-1])
-    f_ippd, f_std = flops(st, False), flops(st, True)
+    tokens = int(st.ctx_start[-1] + st.seg_start[-1]) + (0 if ins is None else int(ins.tok_start[-1]))
+    f_ippd, f_std = flops(st, False, ins), flops(st, True, ins)
     achieved = f_ippd / t_ippd / 1e12
     res = {
         "metric": "stacked-prompt prefill attention: header tokens/s, 1 MI355X",
@@ -145,7 +170,8 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
         "data": "synthetic (seeded normal K/V/Q, rounded to bf16; no dataset)",
         "config": {"workload": f"{name}: B={wl.num_prompts}, Hq={wl.hq}, Hkv={wl.hkv}, D={wl.head_dim}, "
                                f"Lc={wl.ctx_len}, N={wl.questions}, question tokens "
-                               f"{wl.question_tokens or wl.seg_len}",
+                               f"{wl.question_tokens or wl.seg_len}"
+                               + ("" if ins is None else f", {len(ins.lp)} instructions of {ins.lp.tolist()} tokens"),
                    "header_tokens": tokens, "layers": 1},
         "roofline": {"bound": "mfma", "kernel": "prefill_kernel (one ippd_prefill_attention call)",
                      "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -156,7 +182,7 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
                      "flop_ratio": round(f_std / f_ippd, 3)},
     }
     if cpu_rows > 0:
-        res["cpu_baseline"] = cpu_baseline(st, kv, pq, cpu_rows)
+        res["cpu_baseline"] = cpu_baseline(st, kv, pq, cpu_rows, ins, iq)
     return res
 
 

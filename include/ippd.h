@@ -300,8 +300,19 @@ ippd_status_t standard_decode_step(const ippd_batch_t *batch, const void *q_new,
  * questions of any one prompt (it sizes the grid); a prompt above it sets
  * IPPD_FLAG_BAD_LAYOUT and not all of its question rows are written.
  * active[] is ignored (every question is prefilled).  No workspace; one
- * kernel launch.  Two-level batches (num_instr > 0) are not supported here
- * (IPPD_ERR_SHAPE).
+ * kernel launch.
+ * Two-level batch (num_instr > 0, Sec. 4.4): every question's prompt is
+ * [p_s; c_b; x_i] with p_s the instruction of prompt b.  Then, for token t
+ * of instruction s,
+ *   out_ctx[instr_off[s] + t][h] = the same over the instruction keys 0..t
+ *                                  (causal), query rotated at t;
+ * context rows see all keys of p_s and then their context causally (query
+ * at instr_len[s] + t), question rows all keys of p_s and c_b and then
+ * their own question causally (query at instr_len[s] + ctx_len[b] + u).
+ * q_ctx holds the instruction queries at the instruction rows of the pool
+ * (rows instr_off[s] .. instr_off[s] + instr_len[s] - 1); the cache holds
+ * the instruction keys (ippd_load_instructions).  IPPD computes the rows of
+ * each instruction once.
  */
 ippd_status_t ippd_prefill_attention(const ippd_batch_t *batch, int32_t max_prompt_question_tokens,
                                      const void *q_ctx, const void *q_seg, const ippd_kv_cache_t *kv,
@@ -314,7 +325,9 @@ ippd_status_t ippd_prefill_attention(const ippd_batch_t *batch, int32_t max_prom
  * write the same values to out_ctx).  Same arguments and semantics as
  * ippd_prefill_attention, the bound applying per question, except that the
  * context rows of a prompt without questions are not written (no question's
- * prompt contains them).
+ * prompt contains them), nor, in a two-level batch, the rows of an
+ * instruction none of whose prompts has a question; the instruction rows
+ * are recomputed once per question behind the instruction.
  */
 ippd_status_t standard_prefill_attention(const ippd_batch_t *batch, int32_t max_prompt_question_tokens,
                                          const void *q_ctx, const void *q_seg, const ippd_kv_cache_t *kv,

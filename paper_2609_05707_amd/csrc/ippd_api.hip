@@ -256,9 +256,14 @@ bool plan_prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens, ipp
   const int tb = 16 * rb * waves / G;
   const int64_t n_groups = static_cast<int64_t>(shared ? bt->num_prompts : bt->num_questions) * bt->num_kv_heads;
   const int64_t gps = (n_groups + 7) / 8;
+  // two-level batch: instruction rows once per instruction (IPPD) or per question (baseline)
+  const int S = bt->num_instr;
+  const int64_t n_igroups = S == 0 ? 0 : static_cast<int64_t>(shared ? S : bt->num_questions) * bt->num_kv_heads;
+  const int64_t n_cgroups = n_groups + n_igroups, gps_c = (n_cgroups + 7) / 8;
   const int64_t qtok = shared ? max_q_tokens : (max_q_tokens < bt->seg_capacity ? max_q_tokens : bt->seg_capacity);
-  const int64_t kq = (qtok + tb - 1) / tb, kc = (static_cast<int64_t>(bt->max_ctx_len) + tb - 1) / tb;
-  const int64_t q_blocks = 8 * gps * kq, grid = q_blocks + 8 * gps * kc;
+  const int64_t rows_c = S > 0 && bt->max_instr_len > bt->max_ctx_len ? bt->max_instr_len : bt->max_ctx_len;
+  const int64_t kq = (qtok + tb - 1) / tb, kc = (rows_c + tb - 1) / tb;
+  const int64_t q_blocks = 8 * gps * kq, grid = q_blocks + 8 * gps_c * kc;
   if (grid > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
   pl->waves = waves;
@@ -266,6 +271,8 @@ bool plan_prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens, ipp
   pl->tb = tb;
   pl->n_groups = static_cast<int>(n_groups);
   pl->gps = static_cast<int>(gps);
+  pl->n_cgroups = static_cast<int>(n_cgroups);
+  pl->gps_c = static_cast<int>(gps_c);
   pl->kq = static_cast<int>(kq);
   pl->kc = static_cast<int>(kc);
   pl->q_blocks = static_cast<int>(q_blocks);
@@ -284,7 +291,6 @@ ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens,
   if (!aligned16(q_ctx) || !aligned16(q_seg) || !aligned16(out_ctx) || !aligned16(out_seg) ||
       !aligned16(kv->ctx_k) || !aligned16(kv->ctx_vt) || !aligned16(kv->seg_k) || !aligned16(kv->seg_vt))
     return IPPD_ERR_ALIGN;
-  if (bt->num_instr > 0) return IPPD_ERR_SHAPE;    // the prefill has no instruction level
   ippd::PrefillPlan pl;
   if (!plan_prefill(bt, shared, max_q_tokens, &pl)) return IPPD_ERR_SHAPE;
   if (pl.grid == 0) return IPPD_OK;
@@ -300,6 +306,12 @@ ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens,
   p.max_ctx_len = bt->max_ctx_len;
   p.shared = pl.shared; p.tb = pl.tb; p.n_groups = pl.n_groups; p.gps = pl.gps;
   p.kq = pl.kq; p.kc = pl.kc; p.q_blocks = pl.q_blocks;
+  p.n_cgroups = pl.n_cgroups; p.gps_c = pl.gps_c;
+  p.S = bt->num_instr;
+  p.max_instr_len = bt->num_instr > 0 ? bt->max_instr_len : 0;
+  p.instr_start = bt->num_instr > 0 ? bt->instr_start : nullptr;
+  p.instr_off = bt->num_instr > 0 ? bt->instr_off : nullptr;
+  p.instr_len = bt->num_instr > 0 ? bt->instr_len : nullptr;
   p.c = softmax_scale(bt) * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
   return hip_status(ippd::launch_prefill(bt->dtype, bt->head_dim, pl.grid, p, stream));

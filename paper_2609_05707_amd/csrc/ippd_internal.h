@@ -83,9 +83,10 @@ struct StepPlan {
 // which holds every unit of groups g = 8 j + (u & 7).
 struct PrefillPlan {
   int shared, waves, rb, tb;
-  int n_groups, gps;       // groups, and groups per XCD slice (ceil(n_groups / 8))
+  int n_groups, gps;       // question-row groups, and groups per XCD slice (ceil(n_groups / 8))
+  int n_cgroups, gps_c;    // context-row groups: n_groups, then the instruction groups
   int kq, kc;              // question-row and context-row units per group
-  int q_blocks, grid;      // 8 * gps * kq, then + 8 * gps * kc
+  int q_blocks, grid;      // 8 * gps * kq, then + 8 * gps_c * kc
 };
 
 struct PrefillParams {
@@ -99,6 +100,10 @@ struct PrefillParams {
   int64_t pool;
   int B, Nt, Hq, Hkv, G, D, seg_cap, max_ctx_len;
   int shared, tb, n_groups, gps, kq, kc, q_blocks;
+  int n_cgroups, gps_c;
+  // two-level batch (S > 0): instruction s at pool rows instr_off[s] .. + instr_len[s]
+  const int32_t* instr_start; const int64_t* instr_off; const int32_t* instr_len;
+  int S, max_instr_len;
   float c;                 // scale * log2(e)
   double inv_freq[kMaxHalfDim];
 };

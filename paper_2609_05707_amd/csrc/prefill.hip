@@ -27,8 +27,15 @@
 //                       question's rows up to their own token (causal);
 //   context-row units   context tokens k*tb .. (k+1)*tb - 1: context tiles
 //                       up to the block's last token, causal on the diagonal.
+//   instruction-row units (two-level batch, Sec. 4.4) instruction tokens
+//                       k*tb .., causal over the instruction alone.
+// In a two-level batch every prompt behind instruction p is [p; c_b; x_i]:
+// question-row and context-row units first stream p's tiles, all visible,
+// and the positions of c_b and x_i move up by |p|.  IPPD computes p's rows
+// once per instruction; the baseline recomputes them (and the context rows)
+// once per question.
 // Question-row units come first in the grid (each streams a whole context),
-// then context-row units, longest causal block first.  Unit u of either kind
+// then context-row and instruction-row units, longest causal block first.  Unit u of either kind
 // runs on XCD u & 7, which holds every unit of the groups 8j + (u & 7): the
 // units of a group share its tiles through that XCD's L2.  Groups are
 // numbered kv head minor, so each XCD gets its share of every prompt.
@@ -59,11 +66,12 @@ __device__ __forceinline__ int find_question(const int* pre, int n, int tau) {
   return lo;
 }
 
-// Key tile of a unit: context tiles 0..nct-1, then the tiles of questions
-// jlo..jhi (relative to the group's first question) in order.
+// Key tile of a unit: instruction tiles 0..npt-1 (two-level batch), context
+// tiles npt..npt+nct-1, then the tiles of questions jlo..jhi (relative to the
+// group's first question) in order.
 struct TilePos {
   int idx;    // tile index in the unit's sequence
-  int j;      // question of a segment tile (relative), or -1 for a context tile
+  int j;      // question of a segment tile (relative), or -1 for an instruction or context tile
   int tt;     // tile index within that question's tokens
 };
 
@@ -78,38 +86,67 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
   const bool qunit = blk < p.q_blocks;
   const int ub = qunit ? blk : blk - p.q_blocks;
   const int slice = ub & 7, local = ub >> 3;
-  const int kk = local / p.gps, grp = 8 * (local - kk * p.gps) + slice;
-  if (grp >= p.n_groups) return;
+  const int gps = qunit ? p.gps : p.gps_c;
+  const int kk = local / gps, grp = 8 * (local - kk * gps) + slice;
+  if (grp >= (qunit ? p.n_groups : p.n_cgroups)) return;
   const int k = qunit ? kk : p.kc - 1 - kk;
   const int G = p.G, TB = p.tb;
+  // context-row groups past n_groups hold the rows of an instruction
+  const bool irows = grp >= p.n_groups;
+  const int gl = irows ? grp - p.n_groups : grp;
 
-  int b, g, qa, nq;
+  int b, g, qa, nq, s = 0;
   // kv head minor: the XCD slice (group % 8) cycles over kv heads, which
   // carry equal work, rather than over prompts of different lengths
-  if (p.shared) {
-    b = grp / p.Hkv;
-    g = grp - b * p.Hkv;
+  if (irows && p.shared) {
+    s = gl / p.Hkv;
+    g = gl - s * p.Hkv;
+    b = 0;
+    qa = 0;
+    nq = 0;
+  } else if (p.shared) {
+    b = gl / p.Hkv;
+    g = gl - b * p.Hkv;
     qa = p.q_start[b];
     nq = p.q_start[b + 1] - qa;
   } else {
-    qa = grp / p.Hkv;
-    g = grp - qa * p.Hkv;
+    qa = gl / p.Hkv;
+    g = gl - qa * p.Hkv;
     nq = 1;
     b = prompt_of(p.q_start, p.B, qa);
   }
-  if (b >= p.B || qa < 0 || nq < 0 || nq > kMaxQuestionsPerPrompt || qa + nq > p.Nt) {
+  if (b >= p.B || qa < 0 || nq < 0 || nq > kMaxQuestionsPerPrompt || qa + nq > p.Nt || (irows && s >= p.S)) {
     if (threadIdx.x == 0 && k == 0) raise_flag(p.err_flag, kFlagBadLayout);
     return;
   }
-  const int64_t coff = p.ctx_off[b];
-  const int lc = p.ctx_len[b];
-  if (lc < 0 || lc > p.max_ctx_len || (coff & 7) != 0 || coff < 0 || coff + lc > p.pool) {
-    if (threadIdx.x == 0 && k == 0) raise_flag(p.err_flag, kFlagBadLayout);
-    return;
+  if (p.S > 0 && !(irows && p.shared)) s = instr_of_prompt(p.instr_start, p.S, b);
+  // this unit's rows: tokens coff .. coff+lc-1, after lp visible prefix tokens at poff
+  int64_t coff, poff = 0;
+  int lc, lp = 0;
+  if (p.S > 0) {
+    poff = p.instr_off[s];
+    lp = p.instr_len[s];
+    if (lp < 0 || lp > p.max_instr_len || (poff & 7) != 0 || poff < 0 || poff + lp > p.pool) {
+      if (threadIdx.x == 0 && k == 0) raise_flag(p.err_flag, kFlagBadLayout);
+      return;
+    }
+  }
+  if (irows) {
+    coff = poff;
+    lc = lp;
+    poff = 0;
+    lp = 0;
+  } else {
+    coff = p.ctx_off[b];
+    lc = p.ctx_len[b];
+    if (lc < 0 || lc > p.max_ctx_len || (coff & 7) != 0 || coff < 0 || coff + lc > p.pool) {
+      if (threadIdx.x == 0 && k == 0) raise_flag(p.err_flag, kFlagBadLayout);
+      return;
+    }
   }
 
   // question-row units: prefix sums of the group's question lengths
-  int S = 0;
+  int S = 0;                                      // question tokens of the group
   if (qunit) {
     for (int e = threadIdx.x; e < nq; e += 64 * NW) {
       int s = p.seg_len[qa + e];
@@ -171,7 +208,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
       const int u = tc - sh.pre[j];
       rj[rb] = j;
       lim[rb] = u;
-      pos[rb] = static_cast<int64_t>(lc) + u;
+      pos[rb] = static_cast<int64_t>(lp) + lc + u;
       const int64_t r = (static_cast<int64_t>(qa + j) * p.seg_cap + u) * p.Hq + h;
       qsrc[rb] = static_cast<const T*>(p.q_seg) + r * D;
       dst[rb] = p.out_seg + r * D;
@@ -181,7 +218,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
       const int tc = valid[rb] ? t : k * TB;
       rj[rb] = -1;
       lim[rb] = tc;
-      pos[rb] = tc;
+      pos[rb] = static_cast<int64_t>(lp) + tc;
       const int64_t r = (coff + tc) * p.Hq + h;
       qsrc[rb] = static_cast<const T*>(p.q_ctx) + r * D;
       dst[rb] = p.out_ctx + r * D;
@@ -210,16 +247,16 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
     }
   }
 
-  // key range: context tiles, then (question-row units) the questions present
+  // key range: instruction tiles, context tiles, then (question-row units) the questions present
   const int kv_end = qunit ? lc : min(k * TB + TB, lc);
-  const int nct = (kv_end + 31) >> 5;
+  const int npt = (lp + 31) >> 5, nct = (kv_end + 31) >> 5, npc = npt + nct;
   int jlo = 0, jhi = -1, nst = 0;
   if (qunit) {
     jlo = nq == 1 ? 0 : find_question(sh.pre, nq, k * TB);
     jhi = nq == 1 ? 0 : find_question(sh.pre, nq, min(k * TB + TB, S) - 1);
     for (int j = jlo; j <= jhi; ++j) nst += (sh.pre[j + 1] - sh.pre[j] + 31) >> 5;
   }
-  const int ntiles = __builtin_amdgcn_readfirstlane(nct + nst);
+  const int ntiles = __builtin_amdgcn_readfirstlane(npc + nst);
   const int64_t kvoff = static_cast<int64_t>(g) * p.pool * D;
   const T* kctx = static_cast<const T*>(p.ctx_k) + kvoff;
   const T* vctx = static_cast<const T*>(p.ctx_vt) + kvoff;
@@ -231,7 +268,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
   auto next = [&](TilePos tp) {
     ++tp.idx;
     if (tp.j < 0) {
-      if (tp.idx < nct) return tp;
+      if (tp.idx < npc) return tp;
       tp.j = jlo - 1;
       tp.tt = 0;
     } else if (++tp.tt < ((seg_len_of(tp.j) + 31) >> 5)) {
@@ -245,8 +282,10 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
     return tp;
   };
   auto issue = [&](const TilePos& tp, uint32_t stage) {
-    if (tp.j < 0) {
-      issue_tile<T, D, NW, NS>(stage, kctx, vctx, coff + 32ll * tp.idx, coff + kv_end, wave, lane, toff);
+    if (tp.j < 0 && tp.idx < npt) {
+      issue_tile<T, D, NW, NS>(stage, kctx, vctx, poff + 32ll * tp.idx, poff + lp, wave, lane, toff);
+    } else if (tp.j < 0) {
+      issue_tile<T, D, NW, NS>(stage, kctx, vctx, coff + 32ll * (tp.idx - npt), coff + kv_end, wave, lane, toff);
     } else {
       const int64_t so = (static_cast<int64_t>(qa + tp.j) * p.Hkv + g) * p.seg_cap * D;
       issue_tile<T, D, NW, NS>(stage, static_cast<const T*>(p.seg_k) + so, static_cast<const T*>(p.seg_vt) + so,
@@ -254,8 +293,8 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
     }
   };
 
-  // without context tiles the sequence starts at question jlo, which has tokens
-  const TilePos first{0, nct > 0 ? -1 : jlo, 0};
+  // without instruction or context tiles the sequence starts at question jlo, which has tokens
+  const TilePos first{0, npc > 0 ? -1 : jlo, 0};
   // every compiler-issued load has been consumed; from here the only vector
   // memory operations in flight are this wave's tile DMAs, which the waits count
   wait_vmcnt<0>();
@@ -289,10 +328,15 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
     }
     // tile t: valid tokens and each row's visible limit (relative to the tile start)
     int n, l[RB];
-    if (tc.j < 0) {
-      n = min(32, kv_end - 32 * tc.idx);
+    if (tc.j < 0 && tc.idx < npt) {
+      n = min(32, lp - 32 * tc.idx);
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) l[rb] = qunit ? n - 1 : min(lim[rb] - 32 * tc.idx, n - 1);
+      for (int rb = 0; rb < RB; ++rb) l[rb] = n - 1;
+    } else if (tc.j < 0) {
+      const int ci = tc.idx - npt;
+      n = min(32, kv_end - 32 * ci);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) l[rb] = qunit ? n - 1 : min(lim[rb] - 32 * ci, n - 1);
     } else {
       n = min(32, seg_len_of(tc.j) - 32 * tc.tt);
 #pragma unroll

@@ -260,11 +260,13 @@ class DecodeBatch:
            out.data_ptr(), lse_ptr, ws.data_ptr(), wsb, self.stream())
 
     # ------------------------------------------------------------------ prefill
-    def pack_prefill_queries(self, ctx_q, seg_q, seg_len0):
+    def pack_prefill_queries(self, ctx_q, seg_q, seg_len0, instr_q=None):
         """Raw prefill queries in the library layouts: q_ctx [pool][Hq][D] (prompt
-        b's context token t at row ctx_off[b] + t) and q_seg [Nt][seg_capacity][Hq][D]
-        (question i's token u at [i][u]).  ctx_q [sum Lc, Hq, D] and seg_q
-        [sum seg_len0, Hq, D] are packed in prompt / question order."""
+        b's context token t at row ctx_off[b] + t, instruction s's token t at
+        instr_off[s] + t) and q_seg [Nt][seg_capacity][Hq][D] (question i's token
+        u at [i][u]).  ctx_q [sum Lc, Hq, D], seg_q [sum seg_len0, Hq, D] and
+        instr_q [sum instr_len, Hq, D] are packed in prompt / question /
+        instruction order."""
         cq, sq = self.to_dev(ctx_q), self.to_dev(seg_q)
         q_ctx = torch.zeros(self.pool, self.hq, self.D, dtype=self.tdtype, device=self.device)
         src = 0
@@ -272,6 +274,13 @@ class DecodeBatch:
             n, o = int(self.ctx_len[b]), int(self.ctx_off[b])
             q_ctx[o:o + n] = cq[src:src + n]
             src += n
+        if self.S and instr_q is not None:
+            iq = self.to_dev(instr_q)
+            src = 0
+            for s_ in range(self.S):
+                n, o = int(self.instr_len[s_]), int(self.instr_off[s_])
+                q_ctx[o:o + n] = iq[src:src + n]
+                src += n
         nt = max(self.Nt, 1)
         q_seg = torch.zeros(nt, self.seg_cap, self.hq, self.D, dtype=self.tdtype, device=self.device)
         starts = np.concatenate([[0], np.cumsum(np.asarray(seg_len0, dtype=np.int64))])
@@ -289,8 +298,8 @@ class DecodeBatch:
 
     def prefill(self, layer: int, q_ctx: torch.Tensor, q_seg: torch.Tensor, out_ctx: torch.Tensor,
                 out_seg: torch.Tensor, max_prompt_question_tokens: int, standard: bool = False) -> None:
-        """Prefill attention of every context and question token (the segments hold
-        the question tokens: load them with load_segments first)."""
+        """Prefill attention of every instruction, context and question token (the
+        segments hold the question tokens: load them with load_segments first)."""
         fn = L.standard_prefill_attention if standard else L.ippd_prefill_attention
         fn(self.batches[layer], int(max_prompt_question_tokens), q_ctx.data_ptr(), q_seg.data_ptr(),
            self.caches[layer], out_ctx.data_ptr(), out_seg.data_ptr(), self.stream())

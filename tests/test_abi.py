@@ -182,13 +182,16 @@ def test_instruction_level_validation(lib):
         bt = valid_batch(**kw)
         assert decode_status(lib, bt) == status, kw
         assert lib.ippd_load_instructions(ctypes.byref(bt), FAKE, FAKE, ctypes.byref(kv), None) == status, kw
+        for fn in (lib.ippd_prefill_attention, lib.standard_prefill_attention):
+            assert fn(ctypes.byref(bt), 8, FAKE, FAKE, ctypes.byref(kv), FAKE, FAKE, None) == status, kw
     bt = valid_batch()
     assert lib.ippd_load_instructions(ctypes.byref(bt), FAKE, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_SHAPE
     good = valid_batch(num_instr=1, max_instr_len=64, max_instr_questions=4, instr_start=FAKE, instr_off=FAKE,
                        instr_len=FAKE)
     assert lib.ippd_load_instructions(ctypes.byref(good), None, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_NULL
-    assert lib.ippd_prefill_attention(ctypes.byref(good), 8, FAKE, FAKE, ctypes.byref(kv), FAKE, FAKE,
-                                      None) == L.IPPD_ERR_SHAPE
+    # a valid two-level batch passes the prefill's checks up to its pointers
+    assert lib.ippd_prefill_attention(ctypes.byref(good), 8, None, FAKE, ctypes.byref(kv), FAKE, FAKE,
+                                      None) == L.IPPD_ERR_NULL
 
 
 def test_workspace_formula_with_instructions(lib):

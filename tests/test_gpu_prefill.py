@@ -137,3 +137,80 @@ def test_question_bound_violation_is_flagged():
     st, g_ctx, g_seg, r_ctx, r_seg, db, oc_h, os_h = prefill_case(wl, bound=20)
     assert db.err_flag() & L.IPPD_FLAG_BAD_LAYOUT
     assert max_err(g_ctx, r_ctx) <= 2e-2                       # context rows are unaffected
+
+
+TWO_LEVEL = [
+    # (name, seed, dtype, hq, hkv, D, B, ctx range, questions range, question tokens,
+    #  contexts per instruction, |p| range)
+    ("bf16-d128-cpi2", 450, "bf16", 8, 2, 128, 5, (30, 200), (0, 4), (1, 40), 2, (0, 300)),
+    ("bf16-d64-long-instr", 451, "bf16", 8, 2, 64, 4, (1, 90), (1, 3), (0, 30), 3, (100, 400)),
+    ("f32-d128-cpi2", 452, "f32", 8, 2, 128, 3, (20, 100), (1, 3), (1, 20), 2, (40, 150)),
+    ("f32-d64-one-instr", 453, "f32", 4, 2, 64, 3, (10, 70), (0, 3), (1, 25), 3, (1, 90)),
+    # |p| = 52, 60, 6, 0 with 1, 0, 2, 2 questions: an instruction nobody asks
+    # about (the baseline leaves its rows) and an empty instruction
+    ("f32-d64-cpi1-empty", 463, "f32", 4, 2, 64, 4, (10, 70), (0, 2), (1, 25), 1, (0, 60)),
+]
+
+
+@pytest.mark.parametrize("standard", [False, True])
+@pytest.mark.parametrize("case", TWO_LEVEL, ids=[c[0] for c in TWO_LEVEL])
+def test_two_level_prefill_parity(case, standard):
+    """Two-level batch (Sec. 4.4): each question's prompt is [p; c_b; x_i].  Rows
+    of p are causal over p, context rows see all of p, question rows all of p
+    and c_b; every row is checked against the fp64 oracle, and every pool row
+    outside the instructions and contexts keeps its sentinel."""
+    name, wid, dtype, hq, hkv, d, B, ctx, qs, ql, cpi, lp = case
+    log(f"case: two-level prefill {name} standard={standard}")
+    wl = W.custom_workload(wid=wid, dtype=dtype, num_prompts=B, hq=hq, hkv=hkv,
+                           head_dim=d, ctx_len=ctx, questions=qs, question_tokens=0, seg_len=ql,
+                           value_std=0.5 if dtype == "bf16" else 1.0)
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    pq = W.prefill_queries(st)
+    ins = W.instructions(st, cpi, lp)
+    iq = W.instruction_queries(st, ins)
+    cap = max(8, int(st.seg_len0.max()) if st.num_questions else 8)
+    db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
+                     rope_base=wl.rope_base, instr_len=ins.lp.tolist(), instr_prompt_start=ins.prompt_start.tolist())
+    db.load_instructions(0, ins.k, ins.v)
+    db.load_context(0, kv.ctx_k, kv.ctx_v)
+    db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
+    q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0, instr_q=iq)
+    oc, os_ = db.prefill_outputs(fill=SENTINEL)
+    per_prompt = [int(st.seg_len0[st.q_start[b]:st.q_start[b + 1]].sum()) for b in range(wl.num_prompts)]
+    db.prefill(0, q_ctx, q_seg, oc, os_, max(per_prompt + [0]), standard=standard)
+    torch.cuda.synchronize()
+    oc_h, os_h = oc.cpu().numpy(), os_.cpu().numpy()
+    S = len(ins.lp)
+    g_ctx = np.concatenate([oc_h[db.ctx_off[b]: db.ctx_off[b] + st.ctx_len[b]] for b in range(wl.num_prompts)])
+    g_ins = np.concatenate([oc_h[db.instr_off[s]: db.instr_off[s] + ins.lp[s]] for s in range(S)])
+    g_seg = (np.concatenate([os_h[i, : st.seg_len0[i]] for i in range(st.num_questions)])
+             if st.num_questions else np.zeros((0, wl.hq, wl.head_dim)))
+    r_ctx, r_seg, r_ins = P.prefill_standard(kv.ctx_k, kv.ctx_v, pq.ctx_q, st.ctx_start, st.q_start, kv.seg_k,
+                                             kv.seg_v, pq.seg_q, st.seg_start, wl.rope_base,
+                                             instr=(ins.prompt_start, ins.tok_start, ins.k, ins.v, iq))
+    written = np.zeros(db.pool, bool)
+    for b in range(wl.num_prompts):
+        if standard and st.q_count[b] == 0:
+            # no question's prompt holds this context: its rows stay untouched
+            rows = slice(st.ctx_start[b], st.ctx_start[b + 1])
+            assert (g_ctx[rows] == SENTINEL).all()
+            r_ctx[rows] = np.nan
+            continue
+        written[db.ctx_off[b]: db.ctx_off[b] + st.ctx_len[b]] = True
+    for s in range(S):
+        nq = int(st.q_start[ins.prompt_start[s + 1]] - st.q_start[ins.prompt_start[s]])
+        rows = slice(ins.tok_start[s], ins.tok_start[s + 1])
+        if standard and nq == 0:
+            assert (g_ins[rows] == SENTINEL).all()
+            r_ins[rows] = np.nan
+            continue
+        written[db.instr_off[s]: db.instr_off[s] + ins.lp[s]] = True
+    e_ctx, e_seg, e_ins = max_err(g_ctx, r_ctx), max_err(g_seg, r_seg), max_err(g_ins, r_ins)
+    log(f"  instr rows {len(g_ins)} err {e_ins:.3e}; ctx rows {len(g_ctx)} err {e_ctx:.3e}; "
+        f"question rows {len(g_seg)} err {e_seg:.3e}")
+    assert max(e_ctx, e_seg, e_ins) <= tol(dtype)
+    assert (oc_h[~written] == SENTINEL).all()
+    for i in range(st.num_questions):
+        assert (os_h[i, st.seg_len0[i]:] == SENTINEL).all()
+    assert db.err_flag() == 0

@@ -267,3 +267,10 @@ def instructions(st: Structure, contexts_per_instr: int, lp: Tuple[int, int], la
     k = _draw(rng, shape, wl)
     v = _draw(rng, shape, wl)
     return InstructionKV(prompt_start, lens, tok_start, k, v)
+
+
+def instruction_queries(st: Structure, ins: InstructionKV, layer: int = 0) -> np.ndarray:
+    """Raw query vectors of every instruction token (prefill rows), [sum lp, Hq, D]."""
+    wl = st.wl
+    rng = np.random.default_rng([wl.wid, 6, layer])
+    return _draw(rng, (int(ins.tok_start[-1]), wl.hq, wl.head_dim), wl)
