@@ -331,3 +331,26 @@ def test_32layer_sampled(layer):
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec, layer=layer, questions=sel)
     check(st, gpu, ref, rec, f"wl5-L{layer}", qsel=sel)
+
+
+@pytest.mark.parametrize("mode", ["separate", "fused", "standard"])
+def test_maximum_questions_and_group(mode):
+    """The documented maxima together: 1024 questions in one prompt (the length
+    of a prompt's question list) and G = 16 query heads per kv head (a question
+    fills one 16-row MFMA block), bf16 at D = 128, over two steps with about a
+    third of the questions stopping after the first; empty segments included.
+    Sampled questions against the oracle, which computes them one by one."""
+    log(f"case: 1024 questions in one prompt, G=16, mode={mode}")
+    wl = W.custom_workload(wid=260, dtype="bf16", num_prompts=2, hq=32, hkv=2, head_dim=128, steps=2,
+                           value_std=0.5)
+    rng = np.random.default_rng(9)
+    nt = 1025
+    st = W.Structure(wl, np.array([600, 130]), np.array([1024, 1]), rng.integers(0, 24, size=nt),
+                     rng.choice([1, 2], size=nt, p=[1 / 3, 2 / 3]))
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0, 1], [0, 1], kv=kv, fused=mode == "fused", standard=mode == "standard")
+    assert gpu.err == 0
+    picks = sorted(set([0, 1, 15, 16, 511, 512, 1022, 1023, 1024] + rng.integers(0, nt, 40).tolist()))
+    sel = {0: picks, 1: picks}
+    ref = oracle_steps(st, kv, [0, 1], [0, 1], questions=sel)
+    check(st, gpu, ref, [0, 1], f"1024q-G16-{mode}", qsel=sel)

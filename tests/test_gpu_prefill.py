@@ -214,3 +214,28 @@ def test_two_level_prefill_parity(case, standard):
     for i in range(st.num_questions):
         assert (os_h[i, st.seg_len0[i]:] == SENTINEL).all()
     assert db.err_flag() == 0
+
+
+@pytest.mark.parametrize("standard", [False, True])
+def test_prefill_maximum_questions_and_group(standard):
+    """1024 questions of 0..3 tokens in one prompt (the prefill's question
+    list at its length) with G = 16, bf16 at D = 128: sampled rows against the
+    oracle, the rest finite, sentinels past every question's tokens."""
+    log(f"case: prefill 1024 questions, G=16, standard={standard}")
+    wl = W.custom_workload(wid=470, dtype="bf16", num_prompts=1, hq=32, hkv=2, head_dim=128, ctx_len=(300, 300),
+                           questions=(1024, 1024), question_tokens=0, seg_len=(0, 3), value_std=0.5)
+    rng = np.random.default_rng(11)
+    ctx_rows = sorted(set([0, 31, 32, 299] + rng.integers(0, 300, 8).tolist()))
+    st0 = W.make_structure(wl)
+    nseg = int(st0.seg_start[-1])
+    seg_rows = sorted(set([0, nseg - 1] + rng.integers(0, nseg, 60).tolist()))
+    st, g_ctx, g_seg, r_ctx, r_seg, db, oc_h, os_h = prefill_case(wl, standard=standard, ctx_rows=ctx_rows,
+                                                                 seg_rows=seg_rows)
+    assert int((st.seg_len0 == 0).sum()) > 0
+    e_ctx = max_err(g_ctx[ctx_rows], r_ctx[ctx_rows])
+    e_seg = max_err(g_seg[seg_rows], r_seg[seg_rows])
+    log(f"  sampled ctx max err {e_ctx:.3e}, question max err {e_seg:.3e} ({nseg} question tokens)")
+    assert e_ctx <= 2e-2 and e_seg <= 2e-2
+    assert np.isfinite(g_ctx).all() and np.isfinite(g_seg).all()
+    check_unwritten(st, db, oc_h, os_h, standard)
+    assert db.err_flag() == 0
