@@ -14,6 +14,9 @@ layer-level figure: each layer-step decodes one token per active question
 at that layer).  The same steps are then re-run with the standard baseline
 (standard_decode_step, the context re-read once per question) on
 identical KV, and the fp64 oracle is timed on a bounded sample on the host.
+Beside the headline: the separate-call and graph-replay timings, the warm
+figure (one layer buffer cycled) and single calls timed after a 512 MiB
+cache scrub.
 """
 from __future__ import annotations
 
@@ -208,11 +211,11 @@ def main():
             db.seg_len[l].copy_(seg0)
         torch.cuda.synchronize()
 
-    def run(n_steps, standard=False, events=None, separate=False, dense=False):
+    def run(n_steps, standard=False, events=None, separate=False, dense=False, nl=None):
         for t in range(n_steps):
             d = t % data_steps
             set_step_active(d)
-            for l in range(layers):
+            for l in range(layers if nl is None else nl):
                 if events is not None:
                     events[t][l][0].record(stream)
                 if separate or dense:
@@ -223,17 +226,38 @@ def main():
                 if events is not None:
                     events[t][l][1].record(stream)
 
-    def timed(standard=False, separate=False, dense=False):
+    def timed(standard=False, separate=False, dense=False, nl=None):
         reset()
-        run(args.warmup, standard, separate=separate, dense=dense)
+        run(args.warmup, standard, separate=separate, dense=dense, nl=nl)
         reset()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        run(steps, standard, separate=separate, dense=dense)
+        run(steps, standard, separate=separate, dense=dense, nl=nl)
         e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / 1e3
+
+    def scrubbed_call_time():
+        """Cross-check of the cold figure: layer 0 only, one decode-step call per
+        step timed alone (HIP events around it), after a 512 MiB write that
+        evicts the caches (L2 and the 256 MB Infinity Cache)."""
+        scrub = torch.empty(512 << 20, dtype=torch.uint8, device=db.device)
+        reset()
+        durs = []
+        for t in range(steps):
+            d = t % data_steps
+            set_step_active(d)
+            scrub.fill_(t & 0xFF)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            db.decode_step(0, qs[d], ks[d], vs[d], write_q_rot=False)
+            b.record(stream)
+            torch.cuda.synchronize()
+            durs.append(a.elapsed_time(b) / 1e3)
+        del scrub
+        reset()
+        return float(np.mean(durs))
 
     def kernel_time(standard=False):
         """Average duration of one decode-step call (its two launches), from HIP events
@@ -289,6 +313,12 @@ def main():
 
     t_graph = graph_time()
     flags["graph"] = db.err_flag()
+    # the same steps on one layer buffer only (warm: the step's bytes may stay in
+    # the Infinity Cache between steps), and single calls after a cache scrub
+    t_warm = timed(False, nl=1)
+    flags["warm"] = db.err_flag()
+    t_scrub = scrubbed_call_time()
+    flags["scrubbed"] = db.err_flag()
 
     result = {
         "metric": METRIC,
@@ -313,6 +343,8 @@ def main():
             "us_per_layer_step": round(t_ippd / (steps * layers) * 1e6, 3),
             "separate_calls_us_per_layer_step": round(t_sep / (steps * layers) * 1e6, 3),
             "graph_replay_us_per_layer_step": round(t_graph / (steps * layers) * 1e6, 3),
+            "warm_single_buffer_us_per_layer_step": round(t_warm / steps * 1e6, 3),
+            "scrubbed_single_call_us": round(t_scrub * 1e6, 3),
         },
         "hbm_gbps": round(bytes_total / t_ippd / 1e9, 1),
         "hbm_frac": round(bytes_total / t_ippd / 1e9 / HBM_PEAK_GBPS, 4),
