@@ -267,6 +267,8 @@ class DecodeBatch:
         u at [i][u]).  ctx_q [sum Lc, Hq, D], seg_q [sum seg_len0, Hq, D] and
         instr_q [sum instr_len, Hq, D] are packed in prompt / question /
         instruction order."""
+        if self.S and instr_q is None:
+            raise ValueError("a two-level batch needs the instruction queries (instr_q)")
         cq, sq = self.to_dev(ctx_q), self.to_dev(seg_q)
         q_ctx = torch.zeros(self.pool, self.hq, self.D, dtype=self.tdtype, device=self.device)
         src = 0
@@ -274,7 +276,7 @@ class DecodeBatch:
             n, o = int(self.ctx_len[b]), int(self.ctx_off[b])
             q_ctx[o:o + n] = cq[src:src + n]
             src += n
-        if self.S and instr_q is not None:
+        if self.S:
             iq = self.to_dev(instr_q)
             src = 0
             for s_ in range(self.S):
