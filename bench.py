@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--no-standard", action="store_true", help="skip the standard baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-mask baseline")
+    ap.add_argument("--no-warm", action="store_true",
+                    help="skip the warm single-buffer and scrubbed single-call timings (every call cold)")
     ap.add_argument("--cpu-sample", type=int, default=400, help="question-steps the oracle computes")
     ap.add_argument("--chunk", type=int, default=0, help="context tokens per unit (0 = library default)")
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per context unit (0 = library default)")
@@ -315,10 +317,12 @@ def main():
     flags["graph"] = db.err_flag()
     # the same steps on one layer buffer only (warm: the step's bytes may stay in
     # the Infinity Cache between steps), and single calls after a cache scrub
-    t_warm = timed(False, nl=1)
-    flags["warm"] = db.err_flag()
-    t_scrub = scrubbed_call_time()
-    flags["scrubbed"] = db.err_flag()
+    t_warm = t_scrub = None
+    if not args.no_warm:
+        t_warm = timed(False, nl=1)
+        flags["warm"] = db.err_flag()
+        t_scrub = scrubbed_call_time()
+        flags["scrubbed"] = db.err_flag()
 
     result = {
         "metric": METRIC,
@@ -343,8 +347,8 @@ def main():
             "us_per_layer_step": round(t_ippd / (steps * layers) * 1e6, 3),
             "separate_calls_us_per_layer_step": round(t_sep / (steps * layers) * 1e6, 3),
             "graph_replay_us_per_layer_step": round(t_graph / (steps * layers) * 1e6, 3),
-            "warm_single_buffer_us_per_layer_step": round(t_warm / steps * 1e6, 3),
-            "scrubbed_single_call_us": round(t_scrub * 1e6, 3),
+            "warm_single_buffer_us_per_layer_step": None if t_warm is None else round(t_warm / steps * 1e6, 3),
+            "scrubbed_single_call_us": None if t_scrub is None else round(t_scrub * 1e6, 3),
         },
         "hbm_gbps": round(bytes_total / t_ippd / 1e9, 1),
         "hbm_frac": round(bytes_total / t_ippd / 1e9 / HBM_PEAK_GBPS, 4),
