@@ -130,13 +130,25 @@ def read_traffic(workload_id: int):
 # ----------------------------------------------------------------- cpu oracle
 
 def cpu_baseline(st: W.Structure, kv: W.LayerKV, n_samples: int):
-    """Time the fp64 oracle on the first question-steps of the workload (layer 0)."""
-    from oracle import ippd as O
+    """Time the fp64 oracle on the first question-steps of the workload (layer 0)
+    with the BLAS threads it finds, and on the tiny fp32 workload also with one."""
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         threads = 1
+    rec = _oracle_timing(st, kv, n_samples)
+    rec.update({"cores": int(threads), "host_cpus": os.cpu_count()})
+    if st.wl.wid == 1 and threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            one = _oracle_timing(st, kv, n_samples)
+        rec["one_thread"] = {"value": one["value"], "unit": "tokens/s", "cores": 1, "seconds": one["seconds"]}
+    return rec
+
+
+def _oracle_timing(st: W.Structure, kv: W.LayerKV, n_samples: int):
+    from oracle import ippd as O
     state = O.KVState.from_packed(kv.seg_k, kv.seg_v, st.seg_start)
     done = 0
     t_total = 0.0
@@ -156,7 +168,7 @@ def cpu_baseline(st: W.Structure, kv: W.LayerKV, n_samples: int):
         state.append(si.k_new, si.v_new, si.active)
         if done >= n_samples:
             break
-    return {"value": done / t_total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+    return {"value": done / t_total, "unit": "tokens/s", "kind": "oracle",
             "sample": f"{done} question-steps of layer 0 (steps 0..{steps_used - 1}, all heads), "
                       f"{t_total:.1f} s of fp64 numpy",
             "seconds": round(t_total, 2)}
