@@ -215,9 +215,9 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
-    def set_step_active(t):
+    def set_step_active(t, nl=None):
         ptr = acts[t % data_steps].data_ptr()
-        for bt in db.batches:
+        for bt in db.batches[: layers if nl is None else nl]:
             bt.active = ptr
 
     def reset():
@@ -228,7 +228,7 @@ def main():
     def run(n_steps, standard=False, events=None, separate=False, dense=False, nl=None):
         for t in range(n_steps):
             d = t % data_steps
-            set_step_active(d)
+            set_step_active(d, nl)
             for l in range(layers if nl is None else nl):
                 if events is not None:
                     events[t][l][0].record(stream)
@@ -261,7 +261,7 @@ def main():
         durs = []
         for t in range(steps):
             d = t % data_steps
-            set_step_active(d)
+            set_step_active(d, 1)
             scrub.fill_(t & 0xFF)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
@@ -301,13 +301,15 @@ def main():
     t_sep = timed(False, separate=True)
     flags = {"ippd": err, "separate": db.err_flag()}
 
-    def graph_time():
+    def graph_time(nl=None):
         """The same steps captured once into a HIP graph and replayed (kernels and
-        arguments of the eager sequence; no host launch cost in the timed region)."""
+        arguments of the eager sequence; no host launch cost in the timed region),
+        over all layer buffers or the first nl."""
         from paper_2609_05707_amd.driver import DecodeLoop
         reset()                                   # the loop restores the lengths it starts from
         loop = DecodeLoop(db, [qs[t % data_steps] for t in range(steps)], [ks[t % data_steps] for t in range(steps)],
-                          [vs[t % data_steps] for t in range(steps)], [acts[t % data_steps] for t in range(steps)])
+                          [vs[t % data_steps] for t in range(steps)], [acts[t % data_steps] for t in range(steps)],
+                          layers=nl)
         loop.capture()
         loop.replay()
         torch.cuda.synchronize()
@@ -328,10 +330,11 @@ def main():
     t_graph = graph_time()
     flags["graph"] = db.err_flag()
     # the same steps on one layer buffer only (warm: the step's bytes may stay in
-    # the Infinity Cache between steps), and single calls after a cache scrub
+    # the Infinity Cache between steps; replayed from a graph, since one call per
+    # step leaves the host's launch cost exposed), and single calls after a cache scrub
     t_warm = t_scrub = None
     if not args.no_warm:
-        t_warm = timed(False, nl=1)
+        t_warm = graph_time(nl=1)
         flags["warm"] = db.err_flag()
         t_scrub = scrubbed_call_time()
         flags["scrubbed"] = db.err_flag()
@@ -359,7 +362,7 @@ def main():
             "us_per_layer_step": round(t_ippd / (steps * layers) * 1e6, 3),
             "separate_calls_us_per_layer_step": round(t_sep / (steps * layers) * 1e6, 3),
             "graph_replay_us_per_layer_step": round(t_graph / (steps * layers) * 1e6, 3),
-            "warm_single_buffer_us_per_layer_step": None if t_warm is None else round(t_warm / steps * 1e6, 3),
+            "warm_single_buffer_graph_us_per_layer_step": None if t_warm is None else round(t_warm / steps * 1e6, 3),
             "scrubbed_single_call_us": None if t_scrub is None else round(t_scrub * 1e6, 3),
         },
         "hbm_gbps": round(bytes_total / t_ippd / 1e9, 1),
