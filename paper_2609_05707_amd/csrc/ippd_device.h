@@ -110,9 +110,6 @@ __device__ __forceinline__ int prompt_of(const int32_t* q_start, int B, int i) {
   return lo;
 }
 
-// Virtual position of prompt b's first context token: the length of the
-// instruction it sits behind in a two-level batch (the largest s with
-// instr_start[s] <= b), 0 without an instruction level.
 // Instruction of prompt b in a two-level batch: the largest s in [0, S) with
 // instr_start[s] <= b.
 __device__ __forceinline__ int instr_of_prompt(const int32_t* instr_start, int S, int b) {
@@ -124,6 +121,8 @@ __device__ __forceinline__ int instr_of_prompt(const int32_t* instr_start, int S
   return lo;
 }
 
+// Virtual position of prompt b's first context token: the length of the
+// instruction it sits behind in a two-level batch, 0 without an instruction level.
 __device__ __forceinline__ int64_t instr_pos_base(const int32_t* instr_start, const int32_t* instr_len, int S, int b) {
   return S > 0 ? instr_len[instr_of_prompt(instr_start, S, b)] : 0;
 }

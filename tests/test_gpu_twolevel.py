@@ -121,3 +121,37 @@ def test_two_level_equals_folded_instruction():
         log(f"  step {t}: max |two-level - folded| = {e:.3e}")
         assert e <= 2e-2
     assert db1.err_flag() == 0 and db2.err_flag() == 0
+
+
+@pytest.mark.parametrize("fault", ["misaligned-offset", "length-over-bound"])
+def test_bad_instruction_layout_is_flagged(fault):
+    """A two-level batch whose instruction table breaks the layout (an offset not
+    a multiple of 8, or a length above max_instr_len) is caught by the kernels'
+    own checks before any access with it: the decode step and both prefill
+    modes raise IPPD_FLAG_BAD_LAYOUT and every kernel exits normally."""
+    from paper_2609_05707_amd import _lib as L
+    log(f"case: two-level bad instruction layout ({fault})")
+    wl = W.custom_workload(wid=630, dtype="bf16", num_prompts=3, hq=8, hkv=2, head_dim=128, ctx_len=(40, 120),
+                           questions=(1, 3), seg_len=(2, 20), steps=1, value_std=0.5)
+    st = W.make_structure(wl)
+    ins = W.instructions(st, 2, (50, 150))
+    db, kv = build(st, ins)
+    if fault == "misaligned-offset":
+        db.d_instr_off[1] = int(db.instr_off[1]) + 3
+    else:
+        db.d_instr_len[0] = int(ins.lp.max()) + 8
+    torch.cuda.synchronize()
+    si = W.step_inputs(st, 0)
+    db.set_active(si.active)
+    db.decode_step(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new))
+    torch.cuda.synchronize()
+    assert db.err_flag() & L.IPPD_FLAG_BAD_LAYOUT
+    pq = W.prefill_queries(st)
+    iq = W.instruction_queries(st, ins)
+    q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0, instr_q=iq)
+    oc, os_ = db.prefill_outputs()
+    for standard in (False, True):
+        db.d_err.zero_()
+        db.prefill(0, q_ctx, q_seg, oc, os_, int(st.seg_len0.sum()), standard=standard)
+        torch.cuda.synchronize()
+        assert db.err_flag() & L.IPPD_FLAG_BAD_LAYOUT, standard
