@@ -18,6 +18,9 @@ Reported per workload (one JSON line each):
                against the dense bf16 MFMA peak of 2500 TFLOP/s;
   standard     the baseline's time, its FLOPs (the context rows recomputed
                once per question) and the IPPD speedup;
+  folded_one_level  (two-level workloads) the IPPD prefill of the same prompts
+               as a one-level batch, each context carrying its own copy of
+               the instruction;
   cpu_baseline the fp64 oracle on a bounded sample of rows (host cores).
 
 Usage: python bench_prefill.py [--workload NAME|all] [--reps 20] [--warmup 3]
@@ -112,6 +115,42 @@ def cpu_baseline(st, kv, pq, budget_rows: int, ins=None, iq=None):
                       f"{dt:.1f} s of fp64 numpy", "seconds": round(dt, 2)}
 
 
+def folded_time(st, kv, pq, ins, iq, reps: int, warmup: int) -> float:
+    """IPPD prefill of the one-level batch in which context b is [p_s; c_b]
+    (the instruction copied into every context behind it)."""
+    import torch
+    from paper_2609_05707_amd.session import DecodeBatch
+    wl = st.wl
+    s_of = np.searchsorted(ins.prompt_start, np.arange(wl.num_prompts), side="right") - 1
+    fk, fv, fq, flen = [], [], [], []
+    for b in range(wl.num_prompts):
+        i0, i1 = ins.tok_start[s_of[b]], ins.tok_start[s_of[b] + 1]
+        c0, c1 = st.ctx_start[b], st.ctx_start[b + 1]
+        fk.append(np.concatenate([ins.k[i0:i1], kv.ctx_k[c0:c1]]))
+        fv.append(np.concatenate([ins.v[i0:i1], kv.ctx_v[c0:c1]]))
+        fq.append(np.concatenate([iq[i0:i1], pq.ctx_q[c0:c1]]))
+        flen.append(len(fk[-1]))
+    db = DecodeBatch(flen, st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype,
+                     max(8, int(st.seg_len0.max())), rope_base=wl.rope_base)
+    db.load_context(0, np.concatenate(fk), np.concatenate(fv))
+    db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
+    q_ctx, q_seg = db.pack_prefill_queries(np.concatenate(fq), pq.seg_q, st.seg_len0)
+    oc, os_ = db.prefill_outputs()
+    bound = max(int(st.seg_len0[st.q_start[b]:st.q_start[b + 1]].sum()) for b in range(wl.num_prompts))
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        db.prefill(0, q_ctx, q_seg, oc, os_, bound)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        db.prefill(0, q_ctx, q_seg, oc, os_, bound)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    assert db.err_flag() == 0
+    return e0.elapsed_time(e1) / 1e3 / reps
+
+
 def run(name: str, reps: int, warmup: int, cpu_rows: int):
     import torch
     from paper_2609_05707_amd.session import DecodeBatch
@@ -154,6 +193,9 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
     t_ippd = timed(False)
     t_std = timed(True)
     assert db.err_flag() == 0
+    folded = None
+    if ins is not None:
+        folded = folded_time(st, kv, pq, ins, iq, reps, warmup)
     tokens = int(st.ctx_start[-1] + st.seg_start[-1]) + (0 if ins is None else int(ins.tok_start[-1]))
     f_ippd, f_std = flops(st, False, ins), flops(st, True, ins)
     achieved = f_ippd / t_ippd / 1e12
@@ -181,6 +223,11 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
                      "achieved_tflops": round(f_std / t_std / 1e12, 1), "ippd_speedup": round(t_std / t_ippd, 3),
                      "flop_ratio": round(f_std / f_ippd, 3)},
     }
+    if folded is not None:
+        res["folded_one_level"] = {
+            "ms_per_call": round(folded * 1e3, 4), "two_level_speedup": round(folded / t_ippd, 3),
+            "note": "the same prompts as a one-level batch whose contexts each carry their own copy of "
+                    "the instruction (IPPD prefill): the instruction rows and tiles once per context"}
     if cpu_rows > 0:
         res["cpu_baseline"] = cpu_baseline(st, kv, pq, cpu_rows, ins, iq)
     return res
