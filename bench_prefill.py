@@ -24,6 +24,11 @@ Reported per workload (one JSON line each):
   cpu_baseline the fp64 oracle on a bounded sample of rows (host cores).
 
 Usage: python bench_prefill.py [--workload NAME|all] [--reps 20] [--warmup 3]
+       python bench_prefill.py --sweep questions|context
+The sweeps are the prefill analogue of the paper's ablations (App. D): one
+Llama-3-8B-shaped prompt with questions of 32 tokens, N = 1..32 questions at
+context 4096, or context 1024..8192 at N = 16; one line per point, then a
+markdown table of the IPPD and standard times.
 """
 from __future__ import annotations
 
@@ -59,6 +64,21 @@ WORKLOADS = {
     "two-level-b8-cpi4-lp2048": dict(wid=503, num_prompts=8, ctx_len=(1024, 1024), questions=(8, 8),
                                      question_tokens=16, seg_len=(0, 0), instr=(4, (2048, 2048))),
 }
+
+
+SWEEP_QUESTIONS = [1, 2, 4, 8, 16, 32]            # at context 4096
+SWEEP_CONTEXT = [1024, 2048, 4096, 8192]           # at N = 16
+
+
+def sweep_points(kind: str):
+    pts = [(n, 4096) for n in SWEEP_QUESTIONS] if kind == "questions" else [(16, lc) for lc in SWEEP_CONTEXT]
+    names = []
+    for n, lc in pts:
+        name = f"sweep-n{n}-lc{lc}"
+        WORKLOADS[name] = dict(wid=520 + n + lc // 256, num_prompts=1, ctx_len=(lc, lc), questions=(n, n),
+                               question_tokens=32, seg_len=(0, 0))
+        names.append((name, n, lc))
+    return names
 
 
 def make(name: str) -> W.DecodeWorkload:
@@ -239,10 +259,23 @@ def main():
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-rows", type=int, default=64, help="rows the oracle computes (0 = skip)")
+    ap.add_argument("--sweep", choices=["questions", "context"], default=None)
     args = ap.parse_args()
     import torch
     assert torch.cuda.is_available(), "bench_prefill.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.sweep:
+        rows = []
+        for name, n, lc in sweep_points(args.sweep):
+            r = run(name, args.reps, args.warmup, 0)
+            print(json.dumps(r), flush=True)
+            rows.append((n, lc, r["ms_per_call"], r["standard"]["ms_per_call"], r["standard"]["ippd_speedup"],
+                         r["standard"]["flop_ratio"], r["roofline"]["achieved"]))
+        print("| N | Lc | IPPD ms | standard ms | speedup | FLOP ratio | IPPD TFLOP/s |")
+        print("|---|---|---|---|---|---|---|")
+        for n, lc, a, b, sp, fr, tf in rows:
+            print(f"| {n} | {lc} | {a:.3f} | {b:.3f} | {sp:.2f} | {fr:.2f} | {tf:.0f} |")
+        return
     names = list(WORKLOADS) if args.workload == "all" else [args.workload]
     for n in names:
         print(json.dumps(run(n, args.reps, args.warmup, args.cpu_rows)), flush=True)
