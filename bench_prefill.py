@@ -171,7 +171,7 @@ def folded_time(st, kv, pq, ins, iq, reps: int, warmup: int) -> float:
     return e0.elapsed_time(e1) / 1e3 / reps
 
 
-def run(name: str, reps: int, warmup: int, cpu_rows: int):
+def run(name: str, reps: int, warmup: int, cpu_rows: int, tile_rows: int = 0):
     import torch
     from paper_2609_05707_amd.session import DecodeBatch
 
@@ -188,7 +188,7 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int):
         iq = W.instruction_queries(st, ins)
         extra = dict(instr_len=ins.lp.tolist(), instr_prompt_start=ins.prompt_start.tolist())
     db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
-                     rope_base=wl.rope_base, **extra)
+                     rope_base=wl.rope_base, tile_rows=tile_rows, **extra)
     if ins is not None:
         db.load_instructions(0, ins.k, ins.v)
     db.load_context(0, kv.ctx_k, kv.ctx_v)
@@ -260,6 +260,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-rows", type=int, default=64, help="rows the oracle computes (0 = skip)")
     ap.add_argument("--sweep", choices=["questions", "context"], default=None)
+    ap.add_argument("--tile-rows", type=int, default=0, help="rows per unit: 128 or 256 (0 = the planner's choice)")
     args = ap.parse_args()
     import torch
     assert torch.cuda.is_available(), "bench_prefill.py needs a GPU"
@@ -267,7 +268,7 @@ def main():
     if args.sweep:
         rows = []
         for name, n, lc in sweep_points(args.sweep):
-            r = run(name, args.reps, args.warmup, 0)
+            r = run(name, args.reps, args.warmup, 0, args.tile_rows)
             print(json.dumps(r), flush=True)
             rows.append((n, lc, r["ms_per_call"], r["standard"]["ms_per_call"], r["standard"]["ippd_speedup"],
                          r["standard"]["flop_ratio"], r["roofline"]["achieved"]))
@@ -278,7 +279,7 @@ def main():
         return
     names = list(WORKLOADS) if args.workload == "all" else [args.workload]
     for n in names:
-        print(json.dumps(run(n, args.reps, args.warmup, args.cpu_rows)), flush=True)
+        print(json.dumps(run(n, args.reps, args.warmup, args.cpu_rows, args.tile_rows)), flush=True)
 
 
 if __name__ == "__main__":

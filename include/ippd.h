@@ -88,7 +88,10 @@ typedef struct ippd_batch {
   int32_t chunk_tokens;      /* context tokens per work unit: 0 = automatic,
                                 else a multiple of 32 (tests use it to vary splits) */
   int32_t tile_rows;         /* query rows per context unit: 0 = automatic, else 16, 32,
-                                64 or 128 (a tuning knob; results do not depend on it) */
+                                64, 128 or 256 (256: bf16 at head_dim 128 only); a tuning
+                                knob, results do not depend on it.  The bf16 head_dim 128
+                                prefill reads 128 and 256 as its unit size and chooses
+                                by itself for any other value */
   double  rope_base;         /* > 0, e.g. 10000 */
   float   scale;             /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
   const int64_t *ctx_off;    /* [B]   pool offset of each context */

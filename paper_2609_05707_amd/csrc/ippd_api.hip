@@ -253,6 +253,18 @@ bool plan_prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens, ipp
   int waves = 0, rb = 0;
   if (!ippd::prefill_variant(bt->dtype, bt->head_dim, &waves, &rb)) return false;
   const int G = bt->num_q_heads / bt->num_kv_heads;
+  // 256-row units that would not fill the chip (an estimate from the host
+  // bounds) are halved: twice the units, each K/V fragment serving one row
+  // block.  tile_rows 128 or 256 fixes the choice.
+  if (rb == 2 && bt->tile_rows == 128) {
+    rb = 1;
+  } else if (rb == 2 && bt->tile_rows != 256) {
+    const int tb2 = 16 * rb * waves / G;
+    const int64_t groups = static_cast<int64_t>(shared ? bt->num_prompts : bt->num_questions) * bt->num_kv_heads;
+    const int64_t qt = shared ? max_q_tokens : (max_q_tokens < bt->seg_capacity ? max_q_tokens : bt->seg_capacity);
+    const int64_t units = groups * ((qt + tb2 - 1) / tb2 + (static_cast<int64_t>(bt->max_ctx_len) + tb2 - 1) / tb2);
+    if (units < compute_units()) rb = 1;
+  }
   const int tb = 16 * rb * waves / G;
   const int64_t n_groups = static_cast<int64_t>(shared ? bt->num_prompts : bt->num_questions) * bt->num_kv_heads;
   const int64_t gps = (n_groups + 7) / 8;
@@ -314,7 +326,7 @@ ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens,
   p.instr_len = bt->num_instr > 0 ? bt->instr_len : nullptr;
   p.c = softmax_scale(bt) * 1.4426950408889634f;
   fill_inv_freq(bt, p.inv_freq);
-  return hip_status(ippd::launch_prefill(bt->dtype, bt->head_dim, pl.grid, p, stream));
+  return hip_status(ippd::launch_prefill(bt->dtype, bt->head_dim, pl.rb, pl.grid, p, stream));
 }
 
 }  // namespace

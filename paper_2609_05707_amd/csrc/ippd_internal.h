@@ -140,10 +140,11 @@ hipError_t launch_merge(const StepParams& p, hipStream_t s);
 // dense-mask baseline: dense_kernel (context-chunk units, then dense segment
 // units) followed by merge_kernel
 hipError_t launch_dense(int dtype, int waves, int rb, int grid, const StepParams& p, hipStream_t s);
-// prefill_kernel for the batch dtype and head dimension (waves / rb fixed per
-// variant: see prefill_variant)
-hipError_t launch_prefill(int dtype, int head_dim, int grid, const PrefillParams& p, hipStream_t s);
-// (waves, rb) of the prefill variant for a dtype and head dimension; false if none
+// prefill_kernel for the batch dtype and head dimension, with rb row blocks
+// per wave (the waves are fixed per dtype and head dimension: see prefill_variant)
+hipError_t launch_prefill(int dtype, int head_dim, int rb, int grid, const PrefillParams& p, hipStream_t s);
+// (waves, rb) of the prefill variant for a dtype and head dimension; false if
+// none.  bf16 at D = 128 also runs with rb = 1.
 bool prefill_variant(int dtype, int head_dim, int* waves, int* rb);
 
 }  // namespace ippd

@@ -378,8 +378,10 @@ __global__ __launch_bounds__(64 * NW, NW >= 8 ? 2 : 1) void prefill_kernel(Prefi
 }
 
 // Variants: bf16 at D = 128 puts two 16-row blocks on each of eight waves
-// (256 rows, every K/V fragment read from LDS serves both); the others use
-// one block per wave.  fp32 at D = 128 has 32 KB stages: four of them.
+// (256 rows, every K/V fragment read from LDS serves both), or one (128
+// rows) when the planner finds too few 256-row units to fill the chip; the
+// others use one block per wave.  fp32 at D = 128 has 32 KB stages: four of
+// them.
 bool prefill_variant(int dtype, int head_dim, int* waves, int* rb) {
   const bool bf = dtype == IPPD_DTYPE_BF16;
   if (head_dim != 64 && head_dim != 128) return false;
@@ -388,9 +390,10 @@ bool prefill_variant(int dtype, int head_dim, int* waves, int* rb) {
   return true;
 }
 
-hipError_t launch_prefill(int dtype, int head_dim, int grid, const PrefillParams& p, hipStream_t s) {
+hipError_t launch_prefill(int dtype, int head_dim, int rb, int grid, const PrefillParams& p, hipStream_t s) {
   const bool bf = dtype == IPPD_DTYPE_BF16;
-  if (bf && head_dim == 128) prefill_kernel<uint16_t, 128, 8, 8, 2><<<grid, 512, 0, s>>>(p);
+  if (bf && head_dim == 128 && rb == 2) prefill_kernel<uint16_t, 128, 8, 8, 2><<<grid, 512, 0, s>>>(p);
+  else if (bf && head_dim == 128) prefill_kernel<uint16_t, 128, 8, 8, 1><<<grid, 512, 0, s>>>(p);
   else if (bf && head_dim == 64) prefill_kernel<uint16_t, 64, 8, 8, 1><<<grid, 512, 0, s>>>(p);
   else if (!bf && head_dim == 128) prefill_kernel<float, 128, 4, 4, 1><<<grid, 256, 0, s>>>(p);
   else if (!bf && head_dim == 64) prefill_kernel<float, 64, 8, 8, 1><<<grid, 512, 0, s>>>(p);

@@ -24,15 +24,16 @@ def tol(dtype):
     return 1e-5 if dtype == "f32" else 2e-2
 
 
-def prefill_case(wl, standard=False, bound=None, ctx_rows=None, seg_rows=None):
+def prefill_case(wl, standard=False, bound=None, ctx_rows=None, seg_rows=None, tile_rows=0):
     """Run one prefill on the GPU; return (structure, gpu_ctx, gpu_seg, ref_ctx, ref_seg, db, oc, os)
-    with GPU rows gathered into the oracle's packed order."""
+    with GPU rows gathered into the oracle's packed order.  tile_rows 128 / 256 fixes
+    the unit size of the bf16 D = 128 kernel (0: the planner's choice)."""
     st = W.make_structure(wl)
     kv = W.layer_kv(st)
     pq = W.prefill_queries(st)
     cap = max(8, int(st.seg_len0.max()) if st.num_questions else 8)
     db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
-                     rope_base=wl.rope_base)
+                     rope_base=wl.rope_base, tile_rows=tile_rows)
     db.load_context(0, kv.ctx_k, kv.ctx_v)
     db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
     q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0)
@@ -75,14 +76,17 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("rows", [0, 128, 256])
 @pytest.mark.parametrize("standard", [False, True])
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_prefill_parity(case, standard):
+def test_prefill_parity(case, standard, rows):
     name, dtype, hq, hkv, d, B, ctx, qs, ql = case
-    log(f"case: prefill {name} standard={standard}")
+    if rows and not (dtype == "bf16" and d == 128):
+        pytest.skip("one unit size for this dtype and head dimension")
+    log(f"case: prefill {name} standard={standard} tile_rows={rows}")
     wl = W.custom_workload(wid=400 + CASES.index(case), dtype=dtype, num_prompts=B, hq=hq, hkv=hkv, head_dim=d,
                            ctx_len=ctx, questions=qs, question_tokens=0, seg_len=ql, value_std=0.5 if dtype == "bf16" else 1.0)
-    st, g_ctx, g_seg, r_ctx, r_seg, db, oc_h, os_h = prefill_case(wl, standard=standard)
+    st, g_ctx, g_seg, r_ctx, r_seg, db, oc_h, os_h = prefill_case(wl, standard=standard, tile_rows=rows)
     if standard:
         # standard prompting runs one prompt per question: the context of a prompt
         # without questions is never prefilled, and its rows stay untouched
@@ -152,15 +156,18 @@ TWO_LEVEL = [
 ]
 
 
+@pytest.mark.parametrize("rows", [0, 256])
 @pytest.mark.parametrize("standard", [False, True])
 @pytest.mark.parametrize("case", TWO_LEVEL, ids=[c[0] for c in TWO_LEVEL])
-def test_two_level_prefill_parity(case, standard):
+def test_two_level_prefill_parity(case, standard, rows):
     """Two-level batch (Sec. 4.4): each question's prompt is [p; c_b; x_i].  Rows
     of p are causal over p, context rows see all of p, question rows all of p
     and c_b; every row is checked against the fp64 oracle, and every pool row
     outside the instructions and contexts keeps its sentinel."""
     name, wid, dtype, hq, hkv, d, B, ctx, qs, ql, cpi, lp = case
-    log(f"case: two-level prefill {name} standard={standard}")
+    if rows and not (dtype == "bf16" and d == 128):
+        pytest.skip("one unit size for this dtype and head dimension")
+    log(f"case: two-level prefill {name} standard={standard} tile_rows={rows}")
     wl = W.custom_workload(wid=wid, dtype=dtype, num_prompts=B, hq=hq, hkv=hkv,
                            head_dim=d, ctx_len=ctx, questions=qs, question_tokens=0, seg_len=ql,
                            value_std=0.5 if dtype == "bf16" else 1.0)
@@ -171,7 +178,8 @@ def test_two_level_prefill_parity(case, standard):
     iq = W.instruction_queries(st, ins)
     cap = max(8, int(st.seg_len0.max()) if st.num_questions else 8)
     db = DecodeBatch(st.ctx_len.tolist(), st.q_count.tolist(), wl.hq, wl.hkv, wl.head_dim, wl.dtype, cap,
-                     rope_base=wl.rope_base, instr_len=ins.lp.tolist(), instr_prompt_start=ins.prompt_start.tolist())
+                     rope_base=wl.rope_base, instr_len=ins.lp.tolist(), instr_prompt_start=ins.prompt_start.tolist(),
+                     tile_rows=rows)
     db.load_instructions(0, ins.k, ins.v)
     db.load_context(0, kv.ctx_k, kv.ctx_v)
     db.load_segments(0, kv.seg_k, kv.seg_v, st.seg_len0)
@@ -216,12 +224,13 @@ def test_two_level_prefill_parity(case, standard):
     assert db.err_flag() == 0
 
 
+@pytest.mark.parametrize("rows", [0, 256])
 @pytest.mark.parametrize("standard", [False, True])
-def test_prefill_maximum_questions_and_group(standard):
+def test_prefill_maximum_questions_and_group(standard, rows):
     """1024 questions of 0..3 tokens in one prompt (the prefill's question
     list at its length) with G = 16, bf16 at D = 128: sampled rows against the
     oracle, the rest finite, sentinels past every question's tokens."""
-    log(f"case: prefill 1024 questions, G=16, standard={standard}")
+    log(f"case: prefill 1024 questions, G=16, standard={standard}, tile_rows={rows}")
     wl = W.custom_workload(wid=470, dtype="bf16", num_prompts=1, hq=32, hkv=2, head_dim=128, ctx_len=(300, 300),
                            questions=(1024, 1024), question_tokens=0, seg_len=(0, 3), value_std=0.5)
     rng = np.random.default_rng(11)
@@ -230,7 +239,7 @@ def test_prefill_maximum_questions_and_group(standard):
     nseg = int(st0.seg_start[-1])
     seg_rows = sorted(set([0, nseg - 1] + rng.integers(0, nseg, 60).tolist()))
     st, g_ctx, g_seg, r_ctx, r_seg, db, oc_h, os_h = prefill_case(wl, standard=standard, ctx_rows=ctx_rows,
-                                                                 seg_rows=seg_rows)
+                                                                 seg_rows=seg_rows, tile_rows=rows)
     assert int((st.seg_len0 == 0).sum()) > 0
     e_ctx = max_err(g_ctx[ctx_rows], r_ctx[ctx_rows])
     e_seg = max_err(g_seg[seg_rows], r_seg[seg_rows])
