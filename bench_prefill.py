@@ -23,7 +23,7 @@ Reported per workload (one JSON line each):
                the instruction;
   cpu_baseline the fp64 oracle on a bounded sample of rows (host cores).
 
-Usage: python bench_prefill.py [--workload NAME|all] [--reps 20] [--warmup 3]
+Usage: python bench_prefill.py [--workload NAME|all] [--reps 30] [--warmup 30]
        python bench_prefill.py --sweep questions|context
 The sweeps are the prefill analogue of the paper's ablations (App. D): one
 Llama-3-8B-shaped prompt with questions of 32 tokens, N = 1..32 questions at
@@ -256,8 +256,8 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int, tile_rows: int = 0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--workload", default="all", choices=["all", *WORKLOADS])
-    ap.add_argument("--reps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--reps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=30, help="untimed calls first (a few leave clocks ramping)")
     ap.add_argument("--cpu-rows", type=int, default=64, help="rows the oracle computes (0 = skip)")
     ap.add_argument("--sweep", choices=["questions", "context"], default=None)
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per unit: 128 or 256 (0 = the planner's choice)")
