@@ -76,13 +76,20 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("rows", [0, 128, 256])
+def _with_unit_sizes(cases, dtype_at, d_at, sizes):
+    """(case, tile_rows) pairs: the bf16 D = 128 kernel at each unit size, the
+    others (one unit size) once."""
+    out = []
+    for c in cases:
+        for r in (sizes if (c[dtype_at] == "bf16" and c[d_at] == 128) else [0]):
+            out.append(pytest.param(c, r, id=f"{c[0]}-rows{r}"))
+    return out
+
+
 @pytest.mark.parametrize("standard", [False, True])
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_prefill_parity(case, standard, rows):
+@pytest.mark.parametrize("case,rows", _with_unit_sizes(CASES, 1, 4, [0, 128, 256]))
+def test_prefill_parity(case, rows, standard):
     name, dtype, hq, hkv, d, B, ctx, qs, ql = case
-    if rows and not (dtype == "bf16" and d == 128):
-        pytest.skip("one unit size for this dtype and head dimension")
     log(f"case: prefill {name} standard={standard} tile_rows={rows}")
     wl = W.custom_workload(wid=400 + CASES.index(case), dtype=dtype, num_prompts=B, hq=hq, hkv=hkv, head_dim=d,
                            ctx_len=ctx, questions=qs, question_tokens=0, seg_len=ql, value_std=0.5 if dtype == "bf16" else 1.0)
@@ -156,17 +163,14 @@ TWO_LEVEL = [
 ]
 
 
-@pytest.mark.parametrize("rows", [0, 256])
 @pytest.mark.parametrize("standard", [False, True])
-@pytest.mark.parametrize("case", TWO_LEVEL, ids=[c[0] for c in TWO_LEVEL])
-def test_two_level_prefill_parity(case, standard, rows):
+@pytest.mark.parametrize("case,rows", _with_unit_sizes(TWO_LEVEL, 2, 5, [0, 256]))
+def test_two_level_prefill_parity(case, rows, standard):
     """Two-level batch (Sec. 4.4): each question's prompt is [p; c_b; x_i].  Rows
     of p are causal over p, context rows see all of p, question rows all of p
     and c_b; every row is checked against the fp64 oracle, and every pool row
     outside the instructions and contexts keeps its sentinel."""
     name, wid, dtype, hq, hkv, d, B, ctx, qs, ql, cpi, lp = case
-    if rows and not (dtype == "bf16" and d == 128):
-        pytest.skip("one unit size for this dtype and head dimension")
     log(f"case: two-level prefill {name} standard={standard} tile_rows={rows}")
     wl = W.custom_workload(wid=wid, dtype=dtype, num_prompts=B, hq=hq, hkv=hkv,
                            head_dim=d, ctx_len=ctx, questions=qs, question_tokens=0, seg_len=ql,
