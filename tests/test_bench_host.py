@@ -47,3 +47,23 @@ def test_step_flops_by_hand():
     expect = 4 * 8 * 64 * ((100 + 3 + 1) + (100 + 5 + 1))
     assert bench.step_flops(st, 0) == expect
     assert bench.step_flops(st, 1) == 0
+
+
+def test_prefill_flops_by_hand():
+    """bench_prefill's algorithmic FLOPs, 4*D*Hq per visible (row, key) pair: one
+    prompt (context 10, questions of 3 and 4 tokens), then behind an instruction
+    of 5 tokens."""
+    import bench_prefill as BP
+    wl = W.custom_workload(wid=901, dtype="bf16", num_prompts=1, hq=8, hkv=2, head_dim=64, steps=1)
+    st = W.Structure(wl, np.array([10]), np.array([2]), np.array([3, 4]), np.array([1, 1]))
+    per = 4 * 64 * 8
+    ctx = 10 * 11 // 2                                  # causal context rows
+    q = (3 * 10 + 3 * 4 // 2) + (4 * 10 + 4 * 5 // 2)   # whole context + causal own question
+    assert BP.flops(st, False) == per * (ctx + q)
+    assert BP.flops(st, True) == per * (2 * ctx + q)   # the context rows once per question
+    ins = W.InstructionKV(np.array([0, 1]), np.array([5]), np.array([0, 5]), None, None)
+    ins_rows = 5 * 6 // 2
+    ctx_i = 10 * 5 + ctx                                # every context row also sees the instruction
+    q_i = (3 * 15 + 3 * 4 // 2) + (4 * 15 + 4 * 5 // 2)
+    assert BP.flops(st, False, ins) == per * (ins_rows + ctx_i + q_i)
+    assert BP.flops(st, True, ins) == per * (2 * ins_rows + 2 * ctx_i + q_i)
