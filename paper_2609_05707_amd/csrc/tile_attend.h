@@ -394,8 +394,11 @@ __device__ __forceinline__ void softmax_pv(const unsigned char* stage, f32x4_t (
 // value fragments are never live together.  On the last iteration stk is
 // any ring stage and sn is not used.  mask(sc[rb], rb) sets the scores of
 // keys a row may not see to -inf; n = valid tokens of tile t (values past
-// them are zeroed, never NaN * 0).
-template <typename T, int D, int NS, int RB, typename MaskFn>
+// them are zeroed, never NaN * 0).  With PRIO the wave raises its priority
+// from its first score product to its last P.V product, so its products
+// issue back to back while the other waves of the SIMD run their softmax or
+// wait for tiles.
+template <typename T, int D, int NS, int RB, bool PRIO = false, typename MaskFn>
 __device__ __forceinline__ void pipe_step_masked(const unsigned char* stk, const unsigned char* stv,
                                                  const typename Mfma<T>::Frag (&qf)[RB][D / 32], f32x4_t (&sc)[RB][2],
                                                  f32x4_t (&sn)[RB][2], RowState<D> (&st)[RB], int n, int lr, int lg,
@@ -420,6 +423,7 @@ __device__ __forceinline__ void pipe_step_masked(const unsigned char* stk, const
   typename M::Frag pf[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) pf[rb] = softmax_step<T, D>(sc[rb], st[rb], c);
+  if (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     f32x4_t acc[RB];
@@ -448,15 +452,18 @@ __device__ __forceinline__ void pipe_step_masked(const unsigned char* stk, const
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) st[rb].o[db] = M::mma(vf[db], pf[rb], st[rb].o[db]);
+  if (PRIO) __builtin_amdgcn_s_setprio(0);
 }
 
-// The decode form: only the tile's tail (tokens >= n) is masked.
+// The decode form: only the tile's tail (tokens >= n) is masked, and the
+// wave's priority is raised over its products (measured faster on decode
+// steps with 64 rows per kv head; the 256-row prefill units gained nothing).
 template <typename T, int D, int NS, int RB>
 __device__ __forceinline__ void pipe_step(const unsigned char* stk, const unsigned char* stv,
                                           const typename Mfma<T>::Frag (&qf)[RB][D / 32], f32x4_t (&sc)[RB][2],
                                           f32x4_t (&sn)[RB][2], RowState<D> (&st)[RB], int n, int lr, int lg,
                                           float c) {
-  pipe_step_masked<T, D, NS, RB>(stk, stv, qf, sc, sn, st, n, lr, lg, c, [n, lg](f32x4_t (&s)[2], int) {
+  pipe_step_masked<T, D, NS, RB, true>(stk, stv, qf, sc, sn, st, n, lr, lg, c, [n, lg](f32x4_t (&s)[2], int) {
     if (n < 32) mask_scores(s, n, lg);
   });
 }
