@@ -227,10 +227,11 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) need = need || l[rb] < 31;
     need = __any(need);
-    pipe_step_masked<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sc, sn,
-                                   rs, n, lr, lg, c, [&](f32x4_t (&x)[2], int rb) {
-                                     if (need) mask_after(x, l[rb], lg);
-                                   });
+    // the decode loop's wave priority, as the IPPD and standard steps have it
+    pipe_step_masked<T, D, NS, RB, true>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf,
+                                         sc, sn, rs, n, lr, lg, c, [&](f32x4_t (&x)[2], int rb) {
+                                           if (need) mask_after(x, l[rb], lg);
+                                         });
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       sc[rb][0] = sn[rb][0];
