@@ -487,6 +487,6 @@ const char* ippd_status_string(ippd_status_t s) {
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 500; }
+int ippd_version(void) { return 600; }
 
 }  // extern "C"

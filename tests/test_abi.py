@@ -189,7 +189,8 @@ def test_instruction_level_validation(lib):
     good = valid_batch(num_instr=1, max_instr_len=64, max_instr_questions=4, instr_start=FAKE, instr_off=FAKE,
                        instr_len=FAKE)
     assert lib.ippd_load_instructions(ctypes.byref(good), None, FAKE, ctypes.byref(kv), None) == L.IPPD_ERR_NULL
-    # a valid two-level batch passes the prefill's checks up to its pointers
+    # a valid two-level batch passes the prefill's checks up to its pointers (0.6.0 on)
+    assert lib.ippd_version() >= 600
     assert lib.ippd_prefill_attention(ctypes.byref(good), 8, None, FAKE, ctypes.byref(kv), FAKE, FAKE,
                                       None) == L.IPPD_ERR_NULL
 
