@@ -180,7 +180,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the decode-attention "
-              "path is measured on a single MI355X and multi-GPU sharding is not part of this build.",
+              "path runs on a single MI355X; sharding over several GPUs is not implemented.",
               file=sys.stderr)
         sys.exit(2)
     import torch
