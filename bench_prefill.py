@@ -22,7 +22,6 @@ Reported per workload (one JSON line each):
   folded_one_level  (two-level workloads) the IPPD prefill of the same prompts
                as a one-level batch, each context carrying its own copy of
                the instruction;
-  cpu_baseline the fp64 oracle on a bounded sample of rows (host cores).
 
 Usage: python bench_prefill.py [--workload NAME|all] [--reps 30] [--warmup 30]
        python bench_prefill.py --sweep questions|context
@@ -113,29 +112,6 @@ def flops(st: W.Structure, standard: bool, ins=None) -> float:
     return tot
 
 
-def cpu_baseline(st, kv, pq, budget_rows: int, ins=None, iq=None):
-    """The fp64 oracle on the first question rows and evenly spaced context rows."""
-    from oracle import prefill as P
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    nc = int(st.ctx_start[-1])
-    ctx_rows = np.linspace(0, nc - 1, num=budget_rows // 2).astype(int).tolist()
-    seg_rows = list(range(min(budget_rows // 2, int(st.seg_start[-1]))))
-    # (a two-level batch also recomputes its instruction rows: they are not counted)
-    instr = None if ins is None else (ins.prompt_start, ins.tok_start, ins.k, ins.v, iq)
-    t0 = time.perf_counter()
-    P.prefill_standard(kv.ctx_k, kv.ctx_v, pq.ctx_q, st.ctx_start, st.q_start, kv.seg_k, kv.seg_v, pq.seg_q,
-                       st.seg_start, st.wl.rope_base, ctx_rows=ctx_rows, seg_rows=seg_rows, instr=instr)
-    dt = time.perf_counter() - t0
-    n = len(ctx_rows) + len(seg_rows)
-    return {"value": n / dt, "unit": "header tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(ctx_rows)} context rows (evenly spaced) + {len(seg_rows)} question rows, all heads, "
-                      f"{dt:.1f} s of fp64 numpy", "seconds": round(dt, 2)}
-
-
 def folded_time(st, kv, pq, ins, iq, reps: int, warmup: int) -> float:
     """IPPD prefill of the one-level batch in which context b is [p_s; c_b]
     (the instruction copied into every context behind it)."""
@@ -172,7 +148,7 @@ def folded_time(st, kv, pq, ins, iq, reps: int, warmup: int) -> float:
     return e0.elapsed_time(e1) / 1e3 / reps
 
 
-def run(name: str, reps: int, warmup: int, cpu_rows: int, tile_rows: int = 0):
+def run(name: str, reps: int, warmup: int, tile_rows: int = 0):
     import torch
     from paper_2609_05707_amd.session import DecodeBatch
 
@@ -256,8 +232,6 @@ def run(name: str, reps: int, warmup: int, cpu_rows: int, tile_rows: int = 0):
             "ms_per_call": round(folded * 1e3, 4), "two_level_speedup": round(folded / t_ippd, 3),
             "note": "the same prompts as a one-level batch whose contexts each carry their own copy of "
                     "the instruction (IPPD prefill): the instruction rows and tiles once per context"}
-    if cpu_rows > 0:
-        res["cpu_baseline"] = cpu_baseline(st, kv, pq, cpu_rows, ins, iq)
     return res
 
 
@@ -266,7 +240,6 @@ def main():
     ap.add_argument("--workload", default="all", choices=["all", *WORKLOADS])
     ap.add_argument("--reps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=30, help="untimed calls first (a few leave clocks ramping)")
-    ap.add_argument("--cpu-rows", type=int, default=64, help="rows the oracle computes (0 = skip)")
     ap.add_argument("--sweep", choices=["questions", "context"], default=None)
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per unit: 128 or 256 (0 = the planner's choice)")
     args = ap.parse_args()
@@ -276,7 +249,7 @@ def main():
     if args.sweep:
         rows = []
         for name, n, lc in sweep_points(args.sweep):
-            r = run(name, args.reps, args.warmup, 0, args.tile_rows)
+            r = run(name, args.reps, args.warmup, args.tile_rows)
             print(json.dumps(r), flush=True)
             rows.append((n, lc, r["ms_per_call"], r["standard"]["ms_per_call"], r["standard"]["ippd_speedup"],
                          r["standard"]["flop_ratio"], r["roofline"]["achieved"]))
@@ -287,7 +260,7 @@ def main():
         return
     names = list(WORKLOADS) if args.workload == "all" else [args.workload]
     for n in names:
-        print(json.dumps(run(n, args.reps, args.warmup, args.cpu_rows, args.tile_rows)), flush=True)
+        print(json.dumps(run(n, args.reps, args.warmup, args.tile_rows)), flush=True)
 
 
 if __name__ == "__main__":
