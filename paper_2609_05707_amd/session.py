@@ -192,7 +192,9 @@ class DecodeBatch:
     def load_segments(self, layer: int, k_packed, v_packed, seg_len0) -> None:
         """k/v_packed: [sum seg_len0, Hkv, D] raw; question i owns the next seg_len0[i] rows."""
         seg_len0 = np.asarray(seg_len0, dtype=np.int64)
-        if self.Nt and int(seg_len0.max()) > self.seg_cap:
+        if self.Nt == 0:
+            return                                      # a batch without questions has no segments
+        if int(seg_len0.max()) > self.seg_cap:
             raise ValueError("initial segment longer than seg_capacity")
         kp, vp = self.to_dev(k_packed), self.to_dev(v_packed)
         nt = max(self.Nt, 1)
