@@ -4,7 +4,7 @@ Each case draws its own small configuration: dtype, head dimension, query
 heads per kv head (1..16), prompts, ragged context / question / segment
 lengths (empty ones included), chunk size, rows per unit, an optional
 instruction level, and the call (fused step, separate calls, standard
-baseline; IPPD or standard prefill).  Every configuration is valid by
+baseline, dense-mask baseline; IPPD or standard prefill).  Every configuration is valid by
 construction.  Tolerances: 1e-5 for fp32, 2e-2 for bf16."""
 import numpy as np
 import pytest
@@ -44,6 +44,10 @@ def draw(k, prefill):
     else:
         cfg["rows"] = int(r.choice([0, 16, 32, 64, 128] + ([256] if dtype == "bf16" and d == 128 else [])))
         cfg["mode"] = str(r.choice(["fused", "separate", "standard"]))
+        # drawn last, so the cases above keep their configurations: the
+        # dense-mask baseline on one-level batches
+        if r.random() < 0.25 and not cfg["two_level"]:
+            cfg["mode"] = "dense"
     return cfg
 
 
@@ -84,9 +88,9 @@ def test_random_decode(k):
         db.set_active(si.active)
         q, kk, v = db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new)
         db.out.fill_(SENTINEL)
-        if cfg["mode"] == "separate":
+        if cfg["mode"] in ("separate", "dense"):
             db.append(0, q, kk, v)
-            db.decode(0)
+            db.decode(0, dense=cfg["mode"] == "dense")
         else:
             db.decode_step(0, q, kk, v, standard=cfg["mode"] == "standard")
         torch.cuda.synchronize()
