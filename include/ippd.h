@@ -108,8 +108,11 @@ typedef struct ippd_batch {
    * occupies pool tokens [instr_off[s], instr_off[s] + instr_len[s]) of the
    * context pool (instr_off a multiple of 8) at positions 0..instr_len[s]-1;
    * the contexts behind it and their questions move up by instr_len[s]
-   * (Sec. 4.1: p at [0, |p|), c_j from |p|).  num_instr = 0 disables the
-   * level and the fields below are not read. */
+   * (Sec. 4.1: p at [0, |p|), c_j from |p|).  A table that breaks these
+   * rules (or puts more than max_instr_questions questions behind one
+   * instruction) sets IPPD_FLAG_BAD_LAYOUT and the decode calls then serve
+   * no question of the batch.  num_instr = 0 disables the level and the
+   * fields below are not read. */
   int32_t num_instr;            /* S >= 0 */
   int32_t max_instr_len;        /* host bound on instr_len[s], <= ctx_pool_tokens */
   int32_t max_instr_questions;  /* host bound on the questions behind one instruction, >= 1 */

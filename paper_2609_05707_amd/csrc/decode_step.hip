@@ -111,6 +111,37 @@ __device__ __forceinline__ PromptInfo find_prompt(const StepParams& p, int i, in
   return r;
 }
 
+// Two-level batch: whether the instruction table is sound (the prompt ranges
+// of the instructions tile [0, B); each instruction lies in the pool and has
+// at most max_instr_questions questions behind it) and question i of prompt
+// b lies in the question range of its instruction: exactly the questions
+// whose instruction slots the instruction units write.  A question for which
+// this fails is skipped (its segment slot carries the skip mark), so that no
+// output is formed from slots nobody wrote.  Whole wave; lane l checks
+// instructions l, l + 64, ...
+__device__ __forceinline__ bool instr_serves(const StepParams& p, int b, int i, int lane) {
+  bool bad = false;
+  for (int s0 = 0; s0 < p.S; s0 += 64) {
+    const int s = s0 + lane;
+    bool lb = false;
+    if (s < p.S) {
+      const int pa = p.instr_start[s], pe = p.instr_start[s + 1];
+      lb = !(pa >= 0 && pe >= pa && pe <= p.B && (s > 0 || pa == 0) && (s < p.S - 1 || pe == p.B));
+      if (!lb) {
+        const int qa = p.q_start[pa], qb = p.q_start[pe];
+        const int64_t off = p.instr_off[s];
+        const int len = p.instr_len[s];
+        lb = !(qa >= 0 && qb >= qa && qb <= p.Nt && qb - qa <= p.max_instr_questions && off >= 0 &&
+               (off & 7) == 0 && len >= 0 && len <= p.max_instr_len && off + len <= p.pool);
+      }
+    }
+    bad = bad || wave_any(lb);
+  }
+  if (bad) return false;
+  const int s = instr_of_prompt(p.instr_start, p.S, b);
+  return p.q_start[p.instr_start[s]] <= i && i < p.q_start[p.instr_start[s + 1]];
+}
+
 // ---------------------------------------------------------------------------
 // Row loads of a context unit: the lane's active flag, segment length and
 // query fragments.  They are issued with inline asm, ahead of the tile DMA,
@@ -228,9 +259,11 @@ __device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], 
 }
 
 // ---------------------------------------------------------------------------
-// LDS of one workgroup.  Context units use main as the tile ring.  Segment
-// units hold, per task, the query rows and the rotation table in it, then
-// the waves' states to be combined.
+// LDS of one workgroup.  Context units use all of it as the tile ring.
+// Segment units (other workgroups) use the same bytes: per task the query
+// rows and the rotation table, then the waves' states to be combined, in the
+// first SEGMAIN bytes, and the per-task last key and value, per-wave (max,
+// sum), per-task last scores and live flags in the small arrays after them.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int NW, int NS>
 struct UnitLds {
@@ -239,13 +272,27 @@ struct UnitLds {
   static constexpr int QAREA = 16 * QROW;                              // one task's query rows
   static constexpr int TASK = QAREA + (D / 2) * 8;                     // + (cos, sin) of its position
   static constexpr int MAIN = RING;
-  static_assert(NW * TASK <= MAIN, "segment tasks must fit");
+  // the segment units' small arrays, at the end of main
+  static constexpr int KV_BYTES = NW * D * static_cast<int>(sizeof(T));
+  static constexpr int EXTRA = 2 * KV_BYTES + NW * 16 * 8 + NW * 16 * 4 + NW * 4;
+  static constexpr int SEGMAIN = (MAIN - EXTRA) & ~15;
+  static_assert(NW * TASK <= SEGMAIN, "segment tasks must fit");
   alignas(16) unsigned char main[MAIN];
-  alignas(16) T k[NW][D];      // per task: the segment's last key (the step's token) and value
-  alignas(16) T v[NW][D];
-  float2 ml[NW][16];           // per wave: (max, sum) of its segment rows
-  float slast[NW][16];         // per task: score of the last key per row
-  int live[NW];                // per task: served this call
+  // per task: the segment's last key (the step's token) and its value
+  __device__ __forceinline__ T* k(int task) { return reinterpret_cast<T*>(main + SEGMAIN) + task * D; }
+  __device__ __forceinline__ T* v(int task) { return reinterpret_cast<T*>(main + SEGMAIN + KV_BYTES) + task * D; }
+  // per wave: (max, sum) of its segment rows
+  __device__ __forceinline__ float2* ml(int wave) {
+    return reinterpret_cast<float2*>(main + SEGMAIN + 2 * KV_BYTES) + wave * 16;
+  }
+  // per task: score of the last key per row
+  __device__ __forceinline__ float* slast(int task) {
+    return reinterpret_cast<float*>(main + SEGMAIN + 2 * KV_BYTES + NW * 16 * 8) + task * 16;
+  }
+  // per task: served this call
+  __device__ __forceinline__ int* live() {
+    return reinterpret_cast<int*>(main + SEGMAIN + 2 * KV_BYTES + NW * 16 * 8 + NW * 16 * 4);
+  }
 };
 
 // ---------------------------------------------------------------------------
@@ -426,7 +473,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
       for (int ds = 0; ds < D / 32; ++ds) qf[rb][ds] = M::zero();
     }
   }
-  const bool live = __any(any_act);                // wave-uniform
+  const bool live = wave_any(any_act);                // wave-uniform
 #pragma unroll
   for (int t = P0; t < RG::NS - 1; ++t)
     if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane, toff);
@@ -444,29 +491,51 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     // P^T V on the MFMA) while the scores of tile t+1 are computed, so each
     // wave has independent MFMA and VALU work in flight.  K of tile t+1 and
     // V of tile t are both in the ring during iteration t.
-    f32x4_t sc[RB][2], sn[RB][2];
+    f32x4_t sa[RB][2], sb[RB][2];
     // tile 0's blocks are this thread's oldest DMAs; tiles 1 .. min(NS-2, last) are younger
     wait_tiles<DPT, RG::NS - 2>(min(last, RG::NS - 2));
     __syncthreads();
-    if (live) qk_tile<T, D, NS, RB>(ring, qf, sc, lr, lg);
-    for (int t = 0; t < ntiles; ++t) {
-      if (t < last) {
-        // tile t+1 must have landed; tiles t+2 .. min(t+NS-2, last) are younger
-        wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
-        __syncthreads();                            // also: every wave is past iteration t-1
-        const int tn = t + RG::NS - 1;
-        if (tn <= last)
-          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
-      }
+    if (live) qk_tile<T, D, NS, RB>(ring, qf, sa, lr, lg);
+    // iteration t < last folds the scores of full tile t and computes those
+    // of tile t+1; unrolled by two so that the two score sets (sa, sb) swap
+    // roles instead of being copied.  The last tile (possibly partial) is
+    // folded after the loop, so the loop carries no masking.  (Written out
+    // rather than as a lambda: a lambda capturing the unit's bases by
+    // reference made the compiler treat them as divergent and move the DMA
+    // addressing to vector registers.)
+    int t = 0;
+    for (; t + 2 <= last; t += 2) {
+      // tile t+1 must have landed; tiles t+2 .. min(t+NS-2, last) are younger
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
+      __syncthreads();                              // also: every wave is past iteration t-1
+      if (t + RG::NS - 1 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 1) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 1), k1, wave, lane, toff);
+      if (live)
+        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sa, sb,
+                                st, 32, lr, lg, c);
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 2, RG::NS - 3));
+      __syncthreads();
+      if (t + RG::NS <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS) % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * (t + RG::NS),
+                                 k1, wave, lane, toff);
+      if (live)
+        pipe_step<T, D, NS, RB>(ring + ((t + 2) % RG::NS) * RG::STAGE, ring + ((t + 1) % RG::NS) * RG::STAGE, qf, sb,
+                                sa, st, 32, lr, lg, c);
+    }
+    if (t < last) {
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
+      __syncthreads();
+      if (t + RG::NS - 1 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 1) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 1), k1, wave, lane, toff);
       if (live) {
-        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sc, sn,
-                                st, t == last ? tail_n : 32, lr, lg, c);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          sc[rb][0] = sn[rb][0];
-          sc[rb][1] = sn[rb][1];
-        }
+        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sa, sb,
+                                st, 32, lr, lg, c);
+        softmax_pv<T, D, NS, RB>(ring + (last % RG::NS) * RG::STAGE, sb, st, tail_n, lr, lg, c);
       }
+    } else if (live) {
+      softmax_pv<T, D, NS, RB>(ring + (last % RG::NS) * RG::STAGE, sa, st, tail_n, lr, lg, c);
     }
   } else {
     for (int t = 0; t < ntiles; ++t) {
@@ -556,7 +625,8 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int s = usable_seg_len(p, sraw);
   if (act && s < 0 && g == 0 && ww == 0 && lane == 0)
     raise_flag(p.err_flag, (p.fused && sraw >= p.seg_cap) ? kFlagSegmentFull : kFlagBadLayout);
-  const bool live = act && s >= 0 && pi.ok;        // bad layouts are flagged by the context units
+  // bad layouts are flagged by the context and instruction units
+  const bool live = act && s >= 0 && pi.ok && (p.S == 0 || instr_serves(p, pi.b, i, lane));
   T* skp = static_cast<T*>(p.seg_k) + sg * p.seg_cap * D;
   T* svp = static_cast<T*>(p.seg_vt) + sg * p.seg_cap * D;     // 8-token column blocks
   const int mem = FUSED ? s : s - 1;               // cached slots before the last key
@@ -565,13 +635,13 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   // sw waves of the task hold states to combine (all tasks' states must fit
   // main); tile t goes to wave (t + 1) % sw, so the leader, busy with the
   // queries first, takes tiles last
-  const int sw = min(wpt, L::MAIN / (G * (D + 4) * 4) / tpu);
+  const int sw = min(wpt, L::SEGMAIN / (G * (D + 4) * 4) / tpu);
   const int first = ww < sw ? (ww + sw - 1) % sw : ntiles;
   unsigned char* qrows = sh.main + k * L::TASK;
   const unsigned char* qrow = qrows + lr * L::QROW + lg * 8 * E;
   Frag kf[2][DS], vf[DB];
   if (ww == 0) {
-    if (lane == 0) sh.live[k] = live ? 1 : 0;
+    if (lane == 0) sh.live()[k] = live ? 1 : 0;
     if (live) {
       // query rows of the G heads (rows >= G zero), rotated at the step
       // token's virtual position ctx_len[b] + seg_len[i] in the fused step
@@ -623,8 +693,8 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
           const T xk = from_f32<T>(x), yk = from_f32<T>(y);
           skp[static_cast<int64_t>(s) * D + jj] = xk;
           skp[static_cast<int64_t>(s) * D + jj + D / 2] = yk;
-          sh.k[k][jj] = xk;
-          sh.k[k][jj + D / 2] = yk;
+          sh.k(k)[jj] = xk;
+          sh.k(k)[jj + D / 2] = yk;
         }
 #pragma unroll
         for (int r = 0; r < (D + 63) / 64; ++r) {
@@ -632,13 +702,13 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
           if (d < D) {
             const T v = vraw[r];
             svp[static_cast<int64_t>(s >> 3) * 8 * D + d * 8 + (s & 7)] = v;
-            sh.v[k][d] = v;
+            sh.v(k)[d] = v;
           }
         }
       } else {
         for (int d = lane; d < D; d += 64) {
-          sh.k[k][d] = skp[static_cast<int64_t>(s - 1) * D + d];
-          sh.v[k][d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
+          sh.k(k)[d] = skp[static_cast<int64_t>(s - 1) * D + d];
+          sh.v(k)[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -649,13 +719,13 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
         const f32x8_t qv = M::to_f32v(M::load(reinterpret_cast<const T*>(qrow + 32 * ds * E)));
-        const f32x8_t kv = M::to_f32v(M::load(&sh.k[k][32 * ds + lg * 8]));
+        const f32x8_t kv = M::to_f32v(M::load(sh.k(k) + 32 * ds + lg * 8));
 #pragma unroll
         for (int uu = 0; uu < 8; ++uu) dot = fmaf(qv[uu], kv[uu], dot);
       }
       dot = xor16_sum(dot);
       dot = xor32_sum(dot);
-      if (lg == 0 && lr < G) sh.slast[k][lr] = dot;
+      if (lg == 0 && lr < G) sh.slast(k)[lr] = dot;
     }
   } else if (first < ntiles) {
     load_seg_tile<T, D>(kf, vf, skp, svp, first, mlast, lr, lg);   // in flight across the barrier
@@ -691,7 +761,7 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
     float* o = reinterpret_cast<float*>(sh.main) + ((k * sw + ww) * G + lr) * (D + 4) + 4 * lg;
 #pragma unroll
     for (int db = 0; db < DB; ++db) *reinterpret_cast<f32x4_t*>(o + 16 * db) = st.o[db];
-    if (lg == 0) sh.ml[k * sw + ww][lr] = make_float2(st.m, st.ls[0]);
+    if (lg == 0) sh.ml(k * sw + ww)[lr] = make_float2(st.m, st.ls[0]);
   }
   __syncthreads();
   // combine each task's wave states and its last key: item (task, row r, dims d0..d0+7)
@@ -701,7 +771,7 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   for (int e = threadIdx.x; e < tpu * per_task; e += 64 * NW) {
     const int kk = e / per_task, er = e - kk * per_task;
     const int r = er / (D / 8), d0 = (er - r * (D / 8)) * 8;
-    if (!sh.live[kk]) {
+    if (!sh.live()[kk]) {
       const int tk = u * tpu + kk;
       if (d0 == 0 && tk < p.Nt * p.Hkv) {
         const int ik = tk / p.Hkv, gk = tk - ik * p.Hkv;
@@ -710,19 +780,19 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
       }
       continue;
     }
-    const float sl = sh.slast[kk][r];
+    const float sl = sh.slast(kk)[r];
     float m = sl;
-    for (int w = 0; w < sw; ++w) m = fmaxf(m, sh.ml[kk * sw + w][r].x);
+    for (int w = 0; w < sw; ++w) m = fmaxf(m, sh.ml(kk * sw + w)[r].x);
     const float fl = fast_exp2((sl - m) * c);
     float lsum = fl;
     f32x4_t a0, a1;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      a0[v] = fl * to_f32<T>(sh.v[kk][d0 + v]);
-      a1[v] = fl * to_f32<T>(sh.v[kk][d0 + 4 + v]);
+      a0[v] = fl * to_f32<T>(sh.v(kk)[d0 + v]);
+      a1[v] = fl * to_f32<T>(sh.v(kk)[d0 + 4 + v]);
     }
     for (int w = 0; w < sw; ++w) {
-      const float2 mlw = sh.ml[kk * sw + w][r];
+      const float2 mlw = sh.ml(kk * sw + w)[r];
       const float f = fast_exp2((mlw.x - m) * c);  // 0 for a wave without tiles (max -inf)
       lsum = fmaf(f, mlw.y, lsum);
       const float* o = reinterpret_cast<const float*>(sh.main) + ((kk * sw + w) * G + r) * (D + 4) + d0;
@@ -811,6 +881,11 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
   const int h = has ? e / (D / 8) : 0, d0 = has ? (e - h * (D / 8)) * 8 : 0;
   const int64_t seg_slot = (static_cast<int64_t>(p.max_chunks) * p.Nt + i) * p.Hq + h;
   const float seg_l = p.part_ml[2 * seg_slot + 1];
+  // dense-mask baseline: its units of a prompt with a bad layout return
+  // without writing, so a question is merged only if its prompt is sound
+  // (the IPPD path's segment units write the skip mark themselves)
+  bool sound = true;
+  if (p.dense) sound = find_prompt(p, i, tid & 63).ok;
   const int s = (p.fused && part == 0 && tid == 0) ? p.seg_len[i] : 0;
   MergeAcc acc;
   acc.init();
@@ -832,7 +907,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
   }
   // every head's segment slot of question i carries the same served/skipped
   // mark, so the decision is workgroup-uniform
-  if (seg_l < 0.f) return;
+  if (seg_l < 0.f || !sound) return;
   if (P > 1) {
     float* dst = mp + tid * 12;
     dst[0] = acc.m;
@@ -869,11 +944,16 @@ static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
 // Ring depth: 4 stages (two workgroups per CU) in general; 8 (one per CU,
 // every tile of a short unit in flight at once) when the context units fit
 // the chip in one wave, or when registers allow one workgroup per CU anyway.
-// fp32 at D = 128 has 32 KB stages: 2 or 4.
+// fp32 at D = 128 has 32 KB stages: 2 or 4.  bf16 at D = 128 (16 KB stages)
+// takes the deepest rings the 160 KB of LDS allow: five stages (80 KB, two
+// workgroups per compute unit) or nine (one workgroup), so that each compute
+// unit keeps six or seven tiles in flight while it computes.
 template <typename T, int D, int NW, int RB>
 static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStream_t s) {
-  constexpr int base = (2 * 32 * D * sizeof(T)) > 16384 ? 2 : 4;
-  return deep ? launch_attend<T, D, NW, 2 * base, RB>(grid, p, s) : launch_attend<T, D, NW, base, RB>(grid, p, s);
+  constexpr int stage = 2 * 32 * D * sizeof(T);
+  constexpr int base = stage > 16384 ? 2 : (stage == 16384 ? 5 : 4);
+  constexpr int dns = stage > 16384 ? 4 : (stage == 16384 ? 9 : 8);
+  return deep ? launch_attend<T, D, NW, dns, RB>(grid, p, s) : launch_attend<T, D, NW, base, RB>(grid, p, s);
 }
 
 template <typename T, int D>

@@ -226,7 +226,7 @@ __global__ __launch_bounds__(64 * NW) void dense_kernel(StepParams p) {
     bool need = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) need = need || l[rb] < 31;
-    need = __any(need);
+    need = wave_any(need);
     // the decode loop's wave priority, as the IPPD and standard steps have it
     pipe_step_masked<T, D, NS, RB, true>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf,
                                          sc, sn, rs, n, lr, lg, c, [&](f32x4_t (&x)[2], int rb) {

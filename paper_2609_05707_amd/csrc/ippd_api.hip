@@ -62,19 +62,14 @@ float softmax_scale(const ippd_batch_t* bt) {
 
 size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-// Compute units of the current device (256 on MI355X); queried once.
-int compute_units() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
-  }
-  return cus;
-}
+// Compute units the planner sizes grids for: the 256 of MI355X (gfx950).  A
+// constant, not a device query, so that the plan (and with it the workspace
+// size) depends on the batch fields only, the library holds no state, and a
+// workspace query on one thread or device agrees with the launch on another.
+// On a part with fewer compute units the plan is still correct, only sized
+// for more of them.
+constexpr int kPlanComputeUnits = 256;
+int compute_units() { return kPlanComputeUnits; }
 
 // theta_j = base^(-2j/D) in fp64, the rotation frequencies of pair j.
 void fill_inv_freq(const ippd_batch_t* bt, double* out) {
@@ -241,6 +236,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   }
   p.scale = softmax_scale(bt);
   p.c = p.scale * 1.4426950408889634f;
+  p.dense = pl.dense;
   fill_inv_freq(bt, p.inv_freq);
   if (pl.dense) return hip_status(ippd::launch_dense(bt->dtype, pl.waves, pl.rb, pl.grid, p, stream));
   return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));

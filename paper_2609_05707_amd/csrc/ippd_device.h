@@ -91,6 +91,12 @@ __device__ __forceinline__ float xor32_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Whether the predicate holds in any active lane.  Built on the ballot
+// intrinsic, whose result the compiler knows to be wave-uniform, so that a
+// branch on it stays a scalar branch and the values computed under it stay
+// in scalar registers.
+__device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
+
 // Values are cached transposed in 8-token column blocks: for a region of n
 // tokens (n a multiple of 8), token t of dimension d sits at
 //   region * n * D + (t / 8) * 8 * D + d * 8 + t % 8,

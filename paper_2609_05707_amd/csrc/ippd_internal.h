@@ -124,6 +124,7 @@ struct StepParams {
   // two-level batch: instruction units (blocks ctx_blocks .. ctx_blocks + instr_blocks - 1)
   const int32_t* instr_start; const int64_t* instr_off; const int32_t* instr_len;
   int S, max_instr_len, max_instr_questions, n_igroups, nrg_i, max_ichunks, instr_blocks;
+  int dense;               // dense-mask baseline (the merge checks each question's prompt)
   int merge_phases;        // threads per merged item (slots split among them), power of 2
   int merge_parts;         // merge workgroups per question
   float c;                 // scale * log2(e)

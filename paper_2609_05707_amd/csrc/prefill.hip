@@ -345,7 +345,7 @@ __device__ __forceinline__ void prefill_unit(const PrefillParams& p, PrefillLds<
     bool need = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) need = need || l[rb] < 31;
-    need = __any(need);
+    need = wave_any(need);
     pipe_step_masked<T, D, NS, RB>(sh.ring + ((t + 1) % RG::NS) * RG::STAGE, sh.ring + (t % RG::NS) * RG::STAGE,
                                    qf, sc, sn, st, n, lr, lg, c, [&](f32x4_t (&s)[2], int rb) {
                                      if (need) mask_after(s, l[rb], lg);

@@ -151,9 +151,12 @@ __device__ __forceinline__ void wait_tiles(int k) {
 }
 
 // One 16-byte LDS-DMA from a wave-uniform base plus this lane's 32-bit
-// offset (the SGPR-base form: no per-lane 64-bit address arithmetic).
+// offset (the SGPR-base form: no per-lane 64-bit address arithmetic).  The
+// compiler cannot see the SGPR read inside the asm, so the asm itself waits
+// out the hazard of a vector instruction having written those SGPRs just
+// before (five wait states: s_nop 4).
 __device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds_block) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(voff), "s"(sbase), "{m0}"(__builtin_amdgcn_readfirstlane(lds_block)) : "memory");
 }
 
@@ -259,7 +262,7 @@ template <typename T, int D>
 __device__ __forceinline__ typename Mfma<T>::Frag softmax_step(const f32x4_t (&sc)[2], RowState<D>& st, float c) {
   const float lmx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
                           fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
-  if (__any((lmx - st.m) * c > kRescaleLog2)) {
+  if (wave_any((lmx - st.m) * c > kRescaleLog2)) {
     float mx = xor16_max(lmx);
     mx = xor32_max(mx);
     const float mn = fmaxf(st.m, mx);

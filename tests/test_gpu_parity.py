@@ -124,21 +124,39 @@ def test_standard_baseline_matches_oracle(dtype, fused):
     check(st, gpu, ref, steps, f"standard-{dtype}-{'fused' if fused else 'sep'}")
 
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_workspace_needs_no_initialisation(fused):
+@pytest.mark.parametrize("mode,fused", [("ippd", False), ("ippd", True), ("standard", False), ("standard", True),
+                                        ("dense", False)])
+def test_workspace_needs_no_initialisation(mode, fused):
     """Every partial state a call reads is written earlier in the same call:
-    a workspace full of NaN bytes gives the oracle's results."""
-    log(f"case: NaN-filled workspace fused={fused}")
+    with the workspace refilled with 0xFF bytes (NaN) before every call, each
+    decode mode gives the oracle's results."""
+    log(f"case: NaN-filled workspace mode={mode} fused={fused}")
     st = W.make_structure(ragged_workload("bf16", 128, steps=3))
     kv = W.layer_kv(st)
     db = make_batch(st, chunk_tokens=64)
     load_layer(db, st, 0, kv)
-    db.ws_ippd.fill_(0xFF)
+    if mode == "dense":
+        db.ws_dense = torch.empty(db.ws_dense_bytes, dtype=torch.uint8, device=db.device)
+    ws = {"ippd": db.ws_ippd, "standard": db.ws_std, "dense": db.ws_dense if mode == "dense" else None}[mode]
     steps = list(range(3))
-    gpu = run_gpu(st, steps, steps, db=db, fused=fused)
     ref = oracle_steps(st, kv, steps, steps)
-    assert gpu.err == 0
-    check(st, gpu, ref, steps, f"nan-workspace-{'fused' if fused else 'sep'}")
+    for t in steps:
+        si = W.step_inputs(st, t)
+        db.set_active(si.active)
+        q, k, v = db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new)
+        ws.fill_(0xFF)
+        if fused:
+            db.decode_step(0, q, k, v, standard=mode == "standard")
+        else:
+            db.append(0, q, k, v)
+            db.decode(0, standard=mode == "standard", dense=mode == "dense")
+        torch.cuda.synchronize()
+        act = st.active(t)
+        eo = max_err(db.out[: st.num_questions].cpu().numpy()[act], ref[t][0][act])
+        el = max_err(db.lse[: st.num_questions].cpu().numpy()[act], ref[t][1][act])
+        log(f"nan-workspace-{mode}-{'fused' if fused else 'sep'} step {t}: out {eo:.3e} lse {el:.3e}")
+        assert eo <= TOL["bf16"] and el <= TOL["bf16"], (mode, t, eo, el)
+    assert db.err_flag() == 0
 
 
 def test_inactive_rows_untouched_and_not_appended():
@@ -252,11 +270,16 @@ def test_all_inactive_step_is_a_noop():
     assert db.err_flag() == 0
 
 
-def test_device_side_flags():
-    log("case: segment overflow and bad layout raise flags, nothing else")
+@pytest.mark.parametrize("mode", ["ippd", "standard", "dense"])
+def test_device_side_flags(mode):
+    """A full segment and a broken prompt layout raise their flags; the
+    questions of the broken prompt get no output row (their rows keep the
+    sentinel) and every other question is still served."""
+    log(f"case: segment overflow and bad layout raise flags, affected rows skipped ({mode})")
     st = W.make_structure(ragged_workload("bf16", 64, steps=1))
     db = make_batch(st, extra_cap=0)
     load_layer(db, st, 0, W.layer_kv(st))
+    seg0 = db.seg_len[0].clone()
     # fill every segment to capacity, then append: overflow flag, seg_len unchanged
     db.seg_len[0][: st.num_questions] = db.seg_cap
     si = W.step_inputs(st, 0)
@@ -265,12 +288,22 @@ def test_device_side_flags():
     torch.cuda.synchronize()
     assert db.err_flag() & 1
     assert int(db.seg_len[0][0]) == db.seg_cap
-    # misaligned context offset: attention skips the prompt and flags it
+    # misaligned context offset of prompt 0: attention skips its questions and flags it
+    db.seg_len[0].copy_(seg0)
+    db.append(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new))
     db.d_err.zero_()
     db.d_ctx_off[0] = 3
-    db.decode(0)
+    db.out.fill_(-777.0)
+    if mode == "dense":
+        db.ws_dense = torch.empty(db.ws_dense_bytes, dtype=torch.uint8, device=db.device)
+        db.ws_dense.fill_(0xFF)
+    db.decode(0, standard=mode == "standard", dense=mode == "dense")
     torch.cuda.synchronize()
     assert db.err_flag() & 2
+    out = db.out[: st.num_questions].cpu().numpy()
+    q0, q1 = int(st.q_start[0]), int(st.q_start[1])
+    assert np.all(out[q0:q1] == -777.0), "rows of the broken prompt were written"
+    assert np.all(np.isfinite(out[q1:])) and not np.any(out[q1:] == -777.0)
 
 
 # -------------------------------------------------------- full-size workloads

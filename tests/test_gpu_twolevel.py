@@ -143,9 +143,19 @@ def test_bad_instruction_layout_is_flagged(fault):
     torch.cuda.synchronize()
     si = W.step_inputs(st, 0)
     db.set_active(si.active)
-    db.decode_step(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new))
-    torch.cuda.synchronize()
-    assert db.err_flag() & L.IPPD_FLAG_BAD_LAYOUT
+    seg0 = db.seg_len[0].clone()
+    for standard in (False, True):
+        # a broken instruction table leaves every question unserved: no row is
+        # formed from instruction slots the instruction units did not write
+        db.seg_len[0].copy_(seg0)
+        db.d_err.zero_()
+        db.out.fill_(SENTINEL)
+        db.ws_ippd.fill_(0xFF)
+        db.ws_std.fill_(0xFF)
+        db.decode_step(0, db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new), standard=standard)
+        torch.cuda.synchronize()
+        assert db.err_flag() & L.IPPD_FLAG_BAD_LAYOUT, standard
+        assert np.all(db.out[: st.num_questions].cpu().numpy() == SENTINEL), standard
     pq = W.prefill_queries(st)
     iq = W.instruction_queries(st, ins)
     q_ctx, q_seg = db.pack_prefill_queries(pq.ctx_q, pq.seg_q, st.seg_len0, instr_q=iq)

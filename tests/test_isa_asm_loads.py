@@ -4,7 +4,15 @@ takes the destination registers as operands.  Correctness then rests on the
 register allocator never reading (or copying) those registers between the
 load and that wait: the data lands there asynchronously.  This test compiles
 decode_step.hip for gfx950 with the library's flags and scans every kernel
-for such an early read.  CPU only (hipcc cross-compiles)."""
+for such an early read.  CPU only (hipcc cross-compiles).
+
+The tile DMAs are inline asm too (global_load_lds_dwordx4 with an SGPR base).
+The compiler cannot see the SGPR read inside the asm, so it does not insert
+the five wait states the hardware needs after a vector instruction writes
+those SGPRs; a base moved there by v_readfirstlane just before the asm was
+read stale and sent a tile DMA to a wild address.  The asm therefore waits
+them out itself (s_nop 4); the DMA tests check that every SGPR-base DMA of
+the three kernel sources does, and that no base is left in VGPRs."""
 import os
 import re
 import shutil
@@ -144,3 +152,46 @@ def test_no_early_reads_of_asm_loads(tmp_path):
     assert "global_load_lds_dwordx4" in asm and ";;#ASMSTART" in asm
     hits = early_reads(asm)
     assert hits == [], hits[:10]
+    assert dma_hazards(asm) == []
+
+
+def dma_hazards(asm: str):
+    """SGPR-base LDS-DMAs of an assembly listing that are not preceded, in
+    their own asm block, by s_nop 4 (or whose base operand is a VGPR)."""
+    bad = []
+    lines = [line.strip() for line in asm.splitlines()]
+    for k, t in enumerate(lines):
+        if not t.startswith("global_load_lds_dwordx4"):
+            continue
+        ops = [f.strip() for f in t.split(None, 1)[1].split(",")]
+        if len(ops) < 2 or ops[1] == "off":
+            continue                                  # per-lane 64-bit address form
+        if not ops[1].startswith("s["):
+            bad.append(("vgpr base", t))
+            continue
+        if k == 0 or lines[k - 1] != "s_nop 4":
+            bad.append(("no wait states", t))
+    return bad
+
+
+def test_dma_hazard_scan_flags_planted_cases():
+    ok = "\n".join([";;#ASMSTART", "s_nop 4", "global_load_lds_dwordx4 v3, s[4:5]", ";;#ASMEND"])
+    assert dma_hazards(ok) == []
+    assert len(dma_hazards(ok.replace("s_nop 4", "s_nop 0"))) == 1
+    assert len(dma_hazards(ok.replace("s[4:5]", "v[4:5]"))) == 1
+    per_lane = "\n".join([";;#ASMSTART", "s_nop 0", "global_load_lds_dwordx4 v[2:3], off", ";;#ASMEND"])
+    assert dma_hazards(per_lane) == []
+
+
+@pytest.mark.skipif(shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"),
+                    reason="hipcc not available")
+@pytest.mark.parametrize("src", ["prefill.hip", "dense_mask.hip"])
+def test_dma_bases_in_sgprs_with_wait_states(tmp_path, src):
+    out = tmp_path / (src + ".s")
+    flags = [f for f in B.flags_for(src) if f != "-fPIC"]
+    cmd = [B.hipcc(), *flags, "--cuda-device-only", "-S", os.path.join(B.CSRC, src), "-o", str(out)]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-2000:]
+    asm = out.read_text()
+    assert "global_load_lds_dwordx4" in asm
+    assert dma_hazards(asm) == []
