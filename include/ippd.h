@@ -52,7 +52,9 @@ typedef enum {
   IPPD_ERR_DTYPE = 3,      /* unknown dtype */
   IPPD_ERR_ALIGN = 4,      /* a data pointer is not 16-byte aligned */
   IPPD_ERR_WORKSPACE = 5,  /* workspace NULL or smaller than required */
-  IPPD_ERR_HIP = 6         /* a HIP launch failed; see ippd_last_hip_error() */
+  IPPD_ERR_HIP = 6,        /* a HIP call failed; see ippd_last_hip_error() */
+  IPPD_ERR_SCRATCH = 7     /* ippd_decode_step_noalloc: the batch needs more than
+                              IPPD_NOALLOC_SCRATCH_BYTES of partial states */
 } ippd_status_t;
 
 /* Bits OR-ed into *err_flag by device code. */
@@ -275,6 +277,27 @@ ippd_status_t ippd_decode_step(const ippd_batch_t *batch, const void *q_new, con
                                const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,
                                float *out, float *lse, void *workspace, size_t workspace_bytes,
                                hipStream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the fused
+ * IPPD decode step of ippd_decode_step with the same arguments, minus the
+ * workspace.  The partial softmax states live instead in a scratch array of
+ * IPPD_NOALLOC_SCRATCH_BYTES that the library holds in device memory on
+ * every GPU it runs on until the process ends.  A batch fits when
+ * ippd_decode_workspace_bytes(batch) <= IPPD_NOALLOC_SCRATCH_BYTES; a larger
+ * one returns IPPD_ERR_SCRATCH before anything is enqueued.  The call
+ * allocates nothing: on the first call on a device it looks up that device's
+ * copy of the array (hipGetSymbolAddress; a failure returns IPPD_ERR_HIP).
+ * `stream` must belong to the current device.  Every call on one GPU shares
+ * that GPU's array, so calls that may run concurrently on one GPU race and
+ * must be ordered (for example on one stream); the array needs no
+ * initialisation and nothing carries from one call to the next.
+ */
+#define IPPD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ippd_status_t ippd_decode_step_noalloc(const ippd_batch_t *batch, const void *q_new, const void *k_new,
+                                       const void *v_new, void *q_rot, const ippd_kv_cache_t *kv,
+                                       float *out, float *lse, hipStream_t stream);
 
 /* The standard baseline as one fused launch (append + per-question attention);
  * workspace >= standard_decode_workspace_bytes(batch). */

@@ -23,6 +23,8 @@ IPPD_ERR_DTYPE = 3
 IPPD_ERR_ALIGN = 4
 IPPD_ERR_WORKSPACE = 5
 IPPD_ERR_HIP = 6
+IPPD_ERR_SCRATCH = 7
+IPPD_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 IPPD_FLAG_SEGMENT_FULL = 1
 IPPD_FLAG_BAD_LAYOUT = 2
@@ -32,7 +34,7 @@ EXPORTED = [
     "ippd_decode_workspace_bytes", "standard_decode_workspace_bytes",
     "ippd_decode_attention", "standard_decode_attention",
     "dense_decode_workspace_bytes", "dense_decode_attention",
-    "ippd_decode_step", "standard_decode_step",
+    "ippd_decode_step", "standard_decode_step", "ippd_decode_step_noalloc",
     "ippd_prefill_attention", "standard_prefill_attention",
     "ippd_status_string", "ippd_last_hip_error", "ippd_version",
 ]
@@ -113,6 +115,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         getattr(lib, name).argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache),
                                        c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
         getattr(lib, name).restype = st
+    lib.ippd_decode_step_noalloc.argtypes = [P(IppdBatch), c_void_p, c_void_p, c_void_p, c_void_p, P(IppdKvCache),
+                                             c_void_p, c_void_p, c_void_p]
+    lib.ippd_decode_step_noalloc.restype = st
     for name in ("ippd_prefill_attention", "standard_prefill_attention"):
         getattr(lib, name).argtypes = [P(IppdBatch), ctypes.c_int32, c_void_p, c_void_p, P(IppdKvCache), c_void_p,
                                        c_void_p, c_void_p]
@@ -191,6 +196,12 @@ def ippd_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, workspace,
     _check("ippd_decode_step",
            load_library().ippd_decode_step(ctypes.byref(batch), q_new, k_new, v_new, q_rot, ctypes.byref(kv),
                                            out, lse, workspace, workspace_bytes, stream))
+
+
+def ippd_decode_step_noalloc(batch, q_new, k_new, v_new, q_rot, kv, out, lse, stream) -> None:
+    _check("ippd_decode_step_noalloc",
+           load_library().ippd_decode_step_noalloc(ctypes.byref(batch), q_new, k_new, v_new, q_rot,
+                                                   ctypes.byref(kv), out, lse, stream))
 
 
 def standard_decode_step(batch, q_new, k_new, v_new, q_rot, kv, out, lse, workspace, workspace_bytes,

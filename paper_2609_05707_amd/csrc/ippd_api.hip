@@ -4,6 +4,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "ippd.h"
 #include "ippd_internal.h"
 
@@ -325,7 +327,18 @@ ippd_status_t prefill(const ippd_batch_t* bt, bool shared, int32_t max_q_tokens,
   return hip_status(ippd::launch_prefill(bt->dtype, bt->head_dim, pl.rb, pl.grid, p, stream));
 }
 
+// Per-device address of the no-allocation scratch array, looked up once per
+// device (concurrent first calls look up the same address).
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
 }  // namespace
+
+// Partial softmax states of ippd_decode_step_noalloc: each GPU the library
+// runs on holds its own copy until the process ends.  In host code this name
+// is a stand-in, not a device address: kernels get the address looked up with
+// hipGetSymbolAddress on the device concerned.
+static __device__ __align__(256) unsigned char scratch[IPPD_NOALLOC_SCRATCH_BYTES];
 
 extern "C" {
 
@@ -448,6 +461,29 @@ ippd_status_t ippd_decode_step(const ippd_batch_t* bt, const void* q_new, const 
                 workspace_bytes, stream);
 }
 
+ippd_status_t ippd_decode_step_noalloc(const ippd_batch_t* bt, const void* q_new, const void* k_new,
+                                       const void* v_new, void* q_rot, const ippd_kv_cache_t* kv, float* out,
+                                       float* lse, hipStream_t stream) {
+  const ippd_status_t st = check_batch(bt);
+  if (st != IPPD_OK) return st;
+  ippd::StepPlan pl;
+  if (!plan_step(bt, true, &pl)) return IPPD_ERR_SHAPE;
+  if (pl.workspace_bytes > IPPD_NOALLOC_SCRATCH_BYTES) return IPPD_ERR_SCRATCH;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return hip_status(hipErrorInvalidDevice);
+  void* ptr = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e);
+    if (ptr == nullptr || (reinterpret_cast<uintptr_t>(ptr) & 255u)) return hip_status(hipErrorInvalidSymbol);
+    g_scratch_addr[dev].store(ptr, std::memory_order_release);
+  }
+  return decode(bt, true, true, q_new, k_new, v_new, nullptr, q_rot, kv, out, lse, ptr, IPPD_NOALLOC_SCRATCH_BYTES,
+                stream);
+}
+
 ippd_status_t standard_decode_step(const ippd_batch_t* bt, const void* q_new, const void* k_new,
                                    const void* v_new, void* q_rot, const ippd_kv_cache_t* kv,
                                    float* out, float* lse, void* workspace, size_t workspace_bytes,
@@ -476,13 +512,14 @@ const char* ippd_status_string(ippd_status_t s) {
     case IPPD_ERR_DTYPE: return "unknown dtype";
     case IPPD_ERR_ALIGN: return "pointer not aligned (16 bytes; workspace 256 bytes)";
     case IPPD_ERR_WORKSPACE: return "workspace missing or too small";
-    case IPPD_ERR_HIP: return "HIP launch failed";
+    case IPPD_ERR_HIP: return "HIP call failed";
+    case IPPD_ERR_SCRATCH: return "batch needs more partial-state scratch than the no-allocation step holds";
   }
   return "unknown status";
 }
 
 int ippd_last_hip_error(void) { return g_last_hip_error; }
 
-int ippd_version(void) { return 600; }
+int ippd_version(void) { return 700; }
 
 }  // extern "C"

@@ -66,7 +66,7 @@ def decode_status(lib, bt, q=FAKE, out=FAKE, ws=FAKE, ws_bytes=None, kv=None, fn
 
 def test_version_and_strings(lib):
     assert lib.ippd_version() >= 100
-    for s in range(7):
+    for s in range(8):
         assert lib.ippd_status_string(s)
     assert lib.ippd_last_hip_error() == 0
 
@@ -219,3 +219,23 @@ def test_dense_baseline_validation(lib):
     two = valid_batch(num_instr=1, max_instr_len=64, max_instr_questions=4, instr_start=FAKE, instr_off=FAKE,
                       instr_len=FAKE)
     assert decode_status(lib, two, fn="dense_decode_attention") == L.IPPD_ERR_SHAPE
+
+
+def test_noalloc_step_rejects_batches_beyond_its_scratch(lib):
+    """ippd_decode_step_noalloc returns IPPD_ERR_SCRATCH, before any HIP call,
+    for a batch whose partial states exceed IPPD_NOALLOC_SCRATCH_BYTES, and
+    validates the batch like the other entry points."""
+    assert lib.ippd_version() >= 700
+    kv = kv_cache()
+    # 1024 questions x 32 heads x (16 context chunks + segment) x 130 floats: far above 64 MiB
+    big = valid_batch(num_questions=1024, max_questions=1024, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                      ctx_pool_tokens=65536, max_ctx_len=65536, chunk_tokens=4096)
+    need = lib.ippd_decode_workspace_bytes(ctypes.byref(big))
+    assert need > L.IPPD_NOALLOC_SCRATCH_BYTES
+    assert lib.ippd_decode_step_noalloc(ctypes.byref(big), FAKE, FAKE, FAKE, FAKE, ctypes.byref(kv), FAKE, None,
+                                        None) == L.IPPD_ERR_SCRATCH
+    assert lib.ippd_status_string(L.IPPD_ERR_SCRATCH)
+    bad = valid_batch(head_dim=96)
+    assert lib.ippd_decode_step_noalloc(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, ctypes.byref(kv), FAKE, None,
+                                        None) == L.IPPD_ERR_SHAPE
+    assert lib.ippd_last_hip_error() == 0
