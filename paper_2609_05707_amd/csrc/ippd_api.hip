@@ -3,6 +3,7 @@
 // caller's stream.
 #include <math.h>
 #include <stdint.h>
+#include <string.h>
 
 #include <atomic>
 
@@ -102,21 +103,32 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
     if (want > sized_rows) sized_rows = want;
   }
   if (rows == 0) rows = sized_rows <= 16 ? 16 : (sized_rows <= 32 ? 32 : (sized_rows <= 64 ? 64 : (sized_rows <= 128 || !two_blocks_ok ? 128 : 256)));
-  int rb = rows > 64 && two_blocks_ok ? 2 : 1;
-  int waves = rows / (16 * rb);
+  // dense-mask units: 16 * rb rows per wave, no parities
+  int dense_rb = rows > 64 && two_blocks_ok ? 2 : 1;
+  int dense_waves = rows / (16 * dense_rb);
   // fp32 at D = 128: the operands of eight waves do not fit their registers
-  if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && waves > 4) waves = 4;
-  const int nrg = static_cast<int>((max_rows + 16 * rb * waves - 1) / (16 * rb * waves));
+  if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && dense_waves > 4) dense_waves = 4;
+  int rb = dense_rb, waves = dense_waves, par = 1;
+  if (two_blocks_ok && rows >= 64) {
+    // bf16 at D = 128: one workgroup of eight waves per compute unit, two
+    // 16-row blocks per wave; units of 256, 128 or 64 rows are 8, 4 or 2
+    // row-waves times 1, 2 or 4 tile parities
+    rb = 2;
+    waves = 8;
+    par = 256 / rows;
+  }
+  const int unit_rows = 16 * rb * waves / par;
+  const int nrg = static_cast<int>((max_rows + unit_rows - 1) / unit_rows);
   // workgroups resident per compute unit (eight waves of two row blocks use
-  // the registers of two)
-  const int wg_per_cu = (rb == 2 && waves == 8) ? 1 : 2;
+  // the registers of two, and their ring the LDS of one)
+  const int wg_per_cu = dense ? ((dense_rb == 2 && dense_waves == 8) ? 1 : 2) : ((rb == 2 && waves == 8) ? 1 : 2);
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   // two-level batch: instruction groups, (instruction, kv head) or (question, kv head)
   const int S = bt->num_instr;
   const int64_t n_igroups = S == 0 ? 0 : (shared ? static_cast<int64_t>(S) : bt->num_questions) * bt->num_kv_heads;
   const int64_t irows = shared ? static_cast<int64_t>(bt->max_instr_questions) * G : G;
-  const int nrg_i = S == 0 ? 1 : static_cast<int>((irows + 16 * rb * waves - 1) / (16 * rb * waves));
+  const int nrg_i = S == 0 ? 1 : static_cast<int>((irows + unit_rows - 1) / unit_rows);
   int chunk = bt->chunk_tokens;
   if (chunk == 0) {
     const int64_t work = n_groups * nrg * bt->max_ctx_len + n_igroups * nrg_i * (S ? bt->max_instr_len : 0);
@@ -151,8 +163,10 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   const int64_t grid = ctx_blocks + instr_blocks + seg_blocks;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) || n_igroups * max_ichunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
-  pl->waves = waves;
-  pl->rb = rb;
+  pl->waves = dense ? dense_waves : waves;
+  pl->rb = dense ? dense_rb : rb;
+  pl->par = dense ? 1 : par;
+  pl->dense_waves = dense_waves;
   pl->nrg = nrg;
   pl->chunk = chunk;
   pl->max_chunks = static_cast<int>(max_chunks);
@@ -241,7 +255,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.dense = pl.dense;
   fill_inv_freq(bt, p.inv_freq);
   if (pl.dense) return hip_status(ippd::launch_dense(bt->dtype, pl.waves, pl.rb, pl.grid, p, stream));
-  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.par, pl.deep != 0, pl.grid, p, stream));
 }
 
 
@@ -505,7 +519,12 @@ ippd_status_t standard_prefill_attention(const ippd_batch_t* bt, int32_t max_pro
 }
 
 const char* ippd_status_string(ippd_status_t s) {
-  switch (s) {
+  // a C caller may pass any int: read it as one (an out-of-range value of the
+  // enum type itself would be undefined behaviour here)
+  int code;
+  static_assert(sizeof(code) == sizeof(s), "status codes are int-sized");
+  memcpy(&code, &s, sizeof code);
+  switch (code) {
     case IPPD_OK: return "ok";
     case IPPD_ERR_NULL: return "required pointer is NULL";
     case IPPD_ERR_SHAPE: return "inconsistent or unsupported sizes";

@@ -29,52 +29,131 @@ __device__ __forceinline__ void rotate8(const T* __restrict__ src, T* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// Decode-step append: one workgroup per question.
+// Decode-step append: one workgroup per question, one 16-byte vector per
+// thread and item.  Item e of question i is
+//   e < Hq*QP                 pairs [v*VE, v*VE + VE) of query head e / QP,
+//                             rotated into q_rot (QP = D/2 / VE pair vectors),
+//   e < (Hq + Hkv)*QP         the same pairs of key head (e - Hq*QP) / QP,
+//                             rotated into segment slot s of (i, head),
+//   e < (Hq + Hkv)*QP + Hkv*VG  dims [v*VE, v*VE + VE) of value head (e - ..) / VG,
+//                             written into slot s of the transposed value cache
+// (VE = 16 bytes / element size, VG = D / VE).  Every load is issued before
+// the question's state is known; the prompt is found with one ballot over
+// the prompts (lane l reads prompt l), so a question costs one round trip of
+// loads and then its stores.  Rotations use the same cos/sin and rounding as
+// the fused decode step, so both give identical bits.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void append_kernel(AppendParams p) {
-  __shared__ float2 s_cs[kMaxHalfDim];
+__global__ __launch_bounds__(1024) void append_kernel(AppendParams p) {
+  constexpr int VE = 16 / static_cast<int>(sizeof(T));
+  typedef T vec_t __attribute__((ext_vector_type(VE)));
   const int i = blockIdx.x;
-  if (i >= p.Nt || !p.active[i]) return;
-  const int b = prompt_of(p.q_start, p.B, i);
+  const int D = p.D, half = D / 2;
+  const int QP = half / VE, VG = D / VE;
+  const int nq = p.Hq * QP, nk = p.Hkv * QP, nitems = nq + nk + p.Hkv * VG;
+  const int lane = threadIdx.x & 63;
+  // the thread's items (a block covers a question in one pass when it can)
+  constexpr int kMaxPass = 2;
+  vec_t lo[kMaxPass], hi[kMaxPass];
+  // theta of the item's VE pairs, read with 16-byte loads before anything
+  // else: one round trip, where per-pair reads of the parameter block would
+  // each wait for the last
+  typedef double th_t __attribute__((ext_vector_type(2)));
+  th_t th[kMaxPass][VE / 2];
+#pragma unroll
+  for (int r = 0; r < kMaxPass; ++r) {
+    const int e = threadIdx.x + r * blockDim.x;
+    const int ee = e < nq ? e : e - nq;
+    const int j0 = e < nq + nk ? (ee % QP) * VE : 0;
+    const th_t* tp = reinterpret_cast<const th_t*>(p.inv_freq + j0);
+#pragma unroll
+    for (int u = 0; u < VE / 2; ++u) th[r][u] = tp[u];
+  }
+  // the question's state, and the first 64 prompts' question ends and
+  // context lengths for the prompt lookup below, all loaded before any wait
+  const bool act = p.active[i] != 0;
   const int s = p.seg_len[i];
+  const int bl0 = lane < p.B ? lane : p.B - 1;
+  const int q10 = p.q_start[bl0 + 1], cl0 = p.ctx_len[bl0];
+  const T* __restrict__ qn = static_cast<const T*>(p.q_new);
+  const T* __restrict__ kn = static_cast<const T*>(p.k_new);
+  const T* __restrict__ vn = static_cast<const T*>(p.v_new);
+  // one load site per pass (a value item reads its vector twice): loads
+  // issued from separate branches into the same registers would each wait
+  // for the one before
+#pragma unroll
+  for (int r = 0; r < kMaxPass; ++r) {
+    const int e = threadIdx.x + r * blockDim.x;
+    const T* src;
+    int hoff;
+    if (e < nq + nk) {
+      const bool isq = e < nq;
+      const int ee = isq ? e : e - nq;
+      src = (isq ? qn + (static_cast<int64_t>(i) * p.Hq + ee / QP) * D
+                 : kn + (static_cast<int64_t>(i) * p.Hkv + ee / QP) * D) + (ee % QP) * VE;
+      hoff = half;
+    } else {
+      const int ev = e - nq - nk;
+      src = vn + (static_cast<int64_t>(i) * p.Hkv + ev / VG) * D + (ev % VG) * VE;
+      hoff = 0;
+    }
+    if (e < nitems) {
+      lo[r] = *reinterpret_cast<const vec_t*>(src);
+      hi[r] = *reinterpret_cast<const vec_t*>(src + hoff);
+    }
+  }
+  // the question's prompt: the number of prompts whose questions all precede
+  // i (windows of 64 prompts; the first was loaded above)
+  int n = __popcll(__ballot(lane < p.B && q10 <= i));
+  int b = n, len = __shfl(cl0, n < 64 ? n : 63, 64);
+  for (int b0 = 64; n == 64 && b0 < p.B; b0 += 64) {
+    const int bb = b0 + lane;
+    const int bl = bb < p.B ? bb : p.B - 1;
+    const int q1 = p.q_start[bl + 1], cl = p.ctx_len[bl];
+    n = __popcll(__ballot(bb < p.B && q1 <= i));
+    b = b0 + n;
+    len = __shfl(cl, n < 64 ? n : 63, 64);
+  }
+  if (b >= p.B) {                                  // i past the last prompt's questions
+    b = p.B - 1;
+    len = p.ctx_len[b];
+  }
+  if (!act) return;
   if (s < 0 || s >= p.seg_cap) {
     if (threadIdx.x == 0) raise_flag(p.err_flag, s >= p.seg_cap ? kFlagSegmentFull : kFlagBadLayout);
     return;
   }
-  const int D = p.D, half = D / 2;
-  const int64_t pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b) + p.ctx_len[b] + s;
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
-    float c, sn;
-    rope_cos_sin(pos, p.inv_freq[j], c, sn);
-    s_cs[j] = make_float2(c, sn);
-  }
-  __syncthreads();
-
-  const T* __restrict__ qn = static_cast<const T*>(p.q_new);
-  const T* __restrict__ kn = static_cast<const T*>(p.k_new);
-  const T* __restrict__ vn = static_cast<const T*>(p.v_new);
+  const int64_t pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b) + len + s;
   T* __restrict__ qr = static_cast<T*>(p.q_rot);
   T* __restrict__ sk = static_cast<T*>(p.seg_k);
   T* __restrict__ svt = static_cast<T*>(p.seg_vt);
-  const int oct = half / 8;                    // groups of 8 pairs per head
-  const int heads = p.Hq + p.Hkv;
-  for (int e = threadIdx.x; e < heads * oct; e += blockDim.x) {
-    const int hh = e / oct, j0 = (e - hh * oct) * 8;
-    if (hh < p.Hq) {
-      const int64_t off = (static_cast<int64_t>(i) * p.Hq + hh) * D;
-      rotate8<T>(qn + off, qr + off, j0, half, s_cs);
-    } else {
-      const int g = hh - p.Hq;
-      const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D;
-      const int64_t dst = ((static_cast<int64_t>(i) * p.Hkv + g) * p.seg_cap + s) * D;
-      rotate8<T>(kn + src, sk + dst, j0, half, s_cs);
+#pragma unroll
+  for (int r = 0; r < kMaxPass; ++r) {
+    const int e = threadIdx.x + r * blockDim.x;
+    if (e < nq + nk) {
+      const bool isq = e < nq;
+      const int ee = isq ? e : e - nq;
+      const int j0 = (ee % QP) * VE;
+      vec_t x, y;
+#pragma unroll
+      for (int u = 0; u < VE; ++u) {
+        float c, sn, xr, yr;
+        rope_cos_sin(pos, th[r][u / 2][u & 1], c, sn);
+        rope_rotate(to_f32<T>(lo[r][u]), to_f32<T>(hi[r][u]), c, sn, xr, yr);
+        x[u] = from_f32<T>(xr);
+        y[u] = from_f32<T>(yr);
+      }
+      T* dst = isq ? qr + (static_cast<int64_t>(i) * p.Hq + ee / QP) * D + j0
+                   : sk + ((static_cast<int64_t>(i) * p.Hkv + ee / QP) * p.seg_cap + s) * D + j0;
+      *reinterpret_cast<vec_t*>(dst) = x;
+      *reinterpret_cast<vec_t*>(dst + half) = y;
+    } else if (e < nitems) {
+      const int ev = e - nq - nk;
+      const int g = ev / VG, d0 = (ev % VG) * VE;
+#pragma unroll
+      for (int u = 0; u < VE; ++u)
+        svt[vt_index(static_cast<int64_t>(i) * p.Hkv + g, p.seg_cap, D, s, d0 + u)] = lo[r][u];
     }
-  }
-  for (int e = threadIdx.x; e < p.Hkv * D; e += blockDim.x) {
-    const int g = e / D, d = e - g * D;
-    const int64_t src = (static_cast<int64_t>(i) * p.Hkv + g) * D + d;
-    svt[vt_index(static_cast<int64_t>(i) * p.Hkv + g, p.seg_cap, D, s, d)] = vn[src];
   }
   __syncthreads();   // every thread has read seg_len[i] before it moves
   if (threadIdx.x == 0) p.seg_len[i] = s + 1;
@@ -199,10 +278,18 @@ hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStrea
   return hipGetLastError();
 }
 
+// One workgroup per question, as many threads (whole waves, at most 1024) as
+// the question has items, or half of them when that exceeds 1024 (each
+// thread then takes two: the kernel covers at most two passes).
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s) {
   if (p.Nt == 0) return hipSuccess;
-  if (dtype == 0) append_kernel<float><<<p.Nt, 256, 0, s>>>(p);
-  else append_kernel<uint16_t><<<p.Nt, 256, 0, s>>>(p);
+  const int ve = dtype == 0 ? 4 : 8;
+  const int items = (p.Hq + p.Hkv) * (p.D / 2 / ve) + p.Hkv * (p.D / ve);
+  int threads = (items + 63) / 64 * 64;
+  if (threads > 1024) threads = ((items + 1) / 2 + 63) / 64 * 64;
+  if (threads > 1024) return hipErrorInvalidValue;
+  if (dtype == 0) append_kernel<float><<<p.Nt, threads, 0, s>>>(p);
+  else append_kernel<uint16_t><<<p.Nt, threads, 0, s>>>(p);
   return hipGetLastError();
 }
 

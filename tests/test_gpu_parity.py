@@ -339,12 +339,14 @@ def test_ragged_b32_sampled():
 
 
 def test_long_context_sampled():
-    log("case: workload 4 (Lc 32768, N 64, 32 steps), sampled questions vs oracle")
+    """Workload 4, the only one with 256-row units: every question at the last
+    step, sampled questions at the first."""
+    log("case: workload 4 (Lc 32768, N 64, 32 steps), all 64 questions at step 31 vs oracle")
     st = W.make_structure(W.workload(4))
     kv = W.layer_kv(st)
     steps = list(range(32))
     rec = [0, 31]
-    sel = {0: [0, 17, 40, 63], 31: [5, 33, 62]}
+    sel = {0: [0, 17, 40, 63], 31: list(range(64))}
     gpu = run_gpu(st, steps, rec, kv=kv, fused=True)
     assert gpu.err == 0
     ref = oracle_steps(st, kv, steps, rec, questions=sel)

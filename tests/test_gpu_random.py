@@ -88,6 +88,7 @@ def test_random_decode(k):
         db.set_active(si.active)
         q, kk, v = db.to_dev(si.q_new), db.to_dev(si.k_new), db.to_dev(si.v_new)
         db.out.fill_(SENTINEL)
+        db.lse.fill_(SENTINEL)
         if cfg["mode"] in ("separate", "dense"):
             db.append(0, q, kk, v)
             db.decode(0, dense=cfg["mode"] == "dense")
@@ -95,14 +96,16 @@ def test_random_decode(k):
             db.decode_step(0, q, kk, v, standard=cfg["mode"] == "standard")
         torch.cuda.synchronize()
         got = db.out[: st.num_questions].float().cpu().numpy()
-        ref, _ = O.decode_step_standard(kv.ctx_k, kv.ctx_v, st.ctx_start, st.q_start, state, si.q_new, si.k_new,
-                                        si.v_new, si.active, wl.rope_base, instr=instr)
+        got_lse = db.lse[: st.num_questions].float().cpu().numpy()
+        ref, ref_lse = O.decode_step_standard(kv.ctx_k, kv.ctx_v, st.ctx_start, st.q_start, state, si.q_new,
+                                              si.k_new, si.v_new, si.active, wl.rope_base, instr=instr)
         state.append(si.k_new, si.v_new, si.active)
         act = si.active
         e = max_err(got[act], ref[act]) if act.any() else 0.0
-        log(f"  step {t}: {int(act.sum())} active, max err {e:.3e}")
-        assert e <= tol(wl.dtype)
-        assert (got[~act] == SENTINEL).all()
+        el = max_err(got_lse[act], ref_lse[act]) if act.any() else 0.0
+        log(f"  step {t}: {int(act.sum())} active, max err out {e:.3e} lse {el:.3e}")
+        assert e <= tol(wl.dtype) and el <= tol(wl.dtype)
+        assert (got[~act] == SENTINEL).all() and (got_lse[~act] == SENTINEL).all()
     np.testing.assert_array_equal(db.seg_len[0][: st.num_questions].cpu().numpy(), st.seg_len_at(wl.steps))
     assert db.err_flag() == 0
 
