@@ -150,6 +150,58 @@ __device__ __forceinline__ bool instr_serves(const StepParams& p, int b, int i, 
 // them, its asm taking the destination registers as operands so that nothing
 // reads them earlier.
 // ---------------------------------------------------------------------------
+// Position of the k-th set bit (k < popcount(m)) of a 64-bit mask, by
+// halving: six rounds of a popcount of the lower half.
+__device__ __forceinline__ int nth_set_bit(uint64_t m, int k) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) {
+    const int c = __popcll(m & ((1ull << w) - 1));
+    if (k >= c) {
+      k -= c;
+      m >>= w;
+      pos += w;
+    }
+  }
+  return pos;
+}
+
+// Active-set compaction of the question range [qa, qb): the number of
+// active questions, and for each of the lane's row blocks the kq[rb]-th of
+// them (-1 if there are fewer).  Questions that have stopped (Sec. 4.2: a
+// finished answer takes no further tokens) then hold no rows, so a unit's
+// rows are the G heads of its prompt's active questions in order.  Whole
+// wave: 64 flags per ballot, four windows per round of loads.
+template <int RB>
+__device__ __forceinline__ int active_questions(const uint8_t* __restrict__ active, int qa, int qb,
+                                                const int (&kq)[RB], int (&qsel)[RB], int lane) {
+  int n = 0;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) qsel[rb] = -1;
+  for (int w0 = qa; w0 < qb; w0 += 256) {
+    // every load unconditional (lanes past qb read flag qb - 1), so that the
+    // four go out together
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = active[min(w0 + 64 * u + lane, qb - 1)];
+    bool f[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f[u] = w0 + 64 * u + lane < qb && v[u] != 0u;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint64_t m = __ballot(f[u]);
+      const int c = __popcll(m);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int k = kq[rb] - n;
+        if (k >= 0 && k < c) qsel[rb] = w0 + 64 * u + nth_set_bit(m, k);
+      }
+      n += c;
+    }
+  }
+  return n;
+}
+
 __device__ __forceinline__ uint32_t gload_u8(const void* p) {
   uint32_t r;
   asm volatile("global_load_ubyte %0, %1, off" : "=v"(r) : "v"(p) : "memory");
@@ -221,12 +273,30 @@ __device__ __forceinline__ void wait_row_loads(RowLoads<T, D, FUSED, RB>& r) {
   for (int k = 0; k < RL::TN; ++k) asm volatile("" : "+v"(r.th[k]));
 }
 
+// Theta of pair u (0..7) of fragment ds from the lane's loaded frequency
+// pieces (piece 4*ds + u/2, double u % 2).
+template <int TN>
+__device__ __forceinline__ double lane_theta(const u32x4_t (&th)[TN], int ds, int u) {
+  const u32x4_t tp = th[4 * ds + u / 2];
+  return __hiloint2double(static_cast<int>(tp[2 * (u & 1) + 1]), static_cast<int>(tp[2 * (u & 1)]));
+}
+
+// Value of lane k of this lane's quad (DPP quad_perm broadcast).
+template <int K>
+__device__ __forceinline__ float quad_bcast(float v) {
+  constexpr int ctrl = K | (K << 2) | (K << 4) | (K << 6);
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), ctrl, 0xF, 0xF, false));
+}
+
 // Query fragments (B operand) of one row block from its loaded pieces,
 // rotated at pos in the fused step.  Pair j < D/2 is (x_j, x_{j+D/2}):
-// fragments ds and ds + DS/2.
+// fragments ds and ds + DS/2.  quad: the four lanes of each lane quad hold
+// heads of one question (G a multiple of 4), so they share every angle:
+// lane k of the quad evaluates pairs k and k + 4 of each fragment and the
+// quad exchanges the rest.
 template <typename T, int D, bool FUSED, int QN, int TN>
 __device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], const u32x4_t (&q)[QN],
-                                          const u32x4_t (&th)[TN], int64_t pos) {
+                                          const u32x4_t (&th)[TN], int64_t pos, bool quad, int lane) {
   using M = Mfma<T>;
   constexpr int DS = D / 32;
 #pragma unroll
@@ -239,22 +309,49 @@ __device__ __forceinline__ void row_query(typename Mfma<T>::Frag (&qf)[D / 32], 
     }
   }
   if constexpr (FUSED) {
+    float cs[DS / 2][8], sn[DS / 2][8];
+    if (quad) {
+      const int k = lane & 3;
 #pragma unroll
-  for (int ds = 0; ds < DS / 2; ++ds) {
-    f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
+      for (int ds = 0; ds < DS / 2; ++ds) {
+        float ca[2], sa[2];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      float cs, sn, xr, yr;
-      const u32x4_t tp = th[4 * ds + u / 2];
-      const double theta = __hiloint2double(static_cast<int>(tp[2 * (u & 1) + 1]), static_cast<int>(tp[2 * (u & 1)]));
-      rope_cos_sin(pos, theta, cs, sn);
-      rope_rotate(x[u], y[u], cs, sn, xr, yr);
-      x[u] = xr;
-      y[u] = yr;
+        for (int hf = 0; hf < 2; ++hf) {
+          // pair k + 4*hf, chosen among the four by value (not by a
+          // runtime index into the pieces, which would go through memory)
+          const double t0 = lane_theta(th, ds, 4 * hf), t1 = lane_theta(th, ds, 4 * hf + 1);
+          const double t2 = lane_theta(th, ds, 4 * hf + 2), t3 = lane_theta(th, ds, 4 * hf + 3);
+          const double t = (k & 2) ? ((k & 1) ? t3 : t2) : ((k & 1) ? t1 : t0);
+          rope_cos_sin(pos, t, ca[hf], sa[hf]);
+        }
+        cs[ds][0] = quad_bcast<0>(ca[0]); sn[ds][0] = quad_bcast<0>(sa[0]);
+        cs[ds][1] = quad_bcast<1>(ca[0]); sn[ds][1] = quad_bcast<1>(sa[0]);
+        cs[ds][2] = quad_bcast<2>(ca[0]); sn[ds][2] = quad_bcast<2>(sa[0]);
+        cs[ds][3] = quad_bcast<3>(ca[0]); sn[ds][3] = quad_bcast<3>(sa[0]);
+        cs[ds][4] = quad_bcast<0>(ca[1]); sn[ds][4] = quad_bcast<0>(sa[1]);
+        cs[ds][5] = quad_bcast<1>(ca[1]); sn[ds][5] = quad_bcast<1>(sa[1]);
+        cs[ds][6] = quad_bcast<2>(ca[1]); sn[ds][6] = quad_bcast<2>(sa[1]);
+        cs[ds][7] = quad_bcast<3>(ca[1]); sn[ds][7] = quad_bcast<3>(sa[1]);
+      }
+    } else {
+#pragma unroll
+      for (int ds = 0; ds < DS / 2; ++ds)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rope_cos_sin(pos, lane_theta(th, ds, u), cs[ds][u], sn[ds][u]);
     }
-    qf[ds] = M::from_f32(x);
-    qf[ds + DS / 2] = M::from_f32(y);
-  }
+#pragma unroll
+    for (int ds = 0; ds < DS / 2; ++ds) {
+      f32x8_t x = M::to_f32v(qf[ds]), y = M::to_f32v(qf[ds + DS / 2]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        float xr, yr;
+        rope_rotate(x[u], y[u], cs[ds][u], sn[ds][u], xr, yr);
+        x[u] = xr;
+        y[u] = yr;
+      }
+      qf[ds] = M::from_f32(x);
+      qf[ds + DS / 2] = M::from_f32(y);
+    }
   }
 }
 
@@ -329,7 +426,9 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   static_assert(NW % PAR == 0, "parities must split the waves");
   constexpr int RWV = NW / PAR;                           // row-waves
   constexpr int RW = 16 * RB * RWV, DPT = RG::BLOCKS / NW;
-  constexpr int P0 = RG::NS - PAR < 3 ? RG::NS - PAR : 3;  // tiles issued before the queries are rotated
+  // tiles issued with the row loads, before the queries are rotated: the
+  // whole ring where the wait count allows
+  constexpr int P0 = RG::NS < 63 / DPT ? RG::NS : 63 / DPT;
   static_assert(RG::NS >= 2 * PAR && P0 >= 1, "the ring must hold two tiles per parity");
   const int par = wave / RWV, rwave = wave - par * RWV;   // wave-uniform
   const int lr = lane & 15, lg = lane >> 4;
@@ -408,9 +507,15 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     if (FUSED && p.S > 0) pos_base = instr_pos_base(p.instr_start, p.instr_len, p.S, b);
   }
   const int G = p.G;
-  const int nrows = (qb - qa) * G;
   const int row0 = rg * RW;
-  if (row0 >= nrows) return;
+  if (row0 >= (qb - qa) * G) return;              // beyond every question's rows
+  // the unit's rows are those of the active questions, compacted: row r is
+  // head g*G + r % G of the (r / G)-th active question of [qa, qb)
+  int kq[RB], qsel[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) kq[rb] = (row0 + 16 * (RB * rwave + rb) + lr) / G;
+  const int nrows = active_questions<RB>(p.active, qa, qb, kq, qsel, lane) * G;
+  if (row0 >= nrows) return;                       // no active rows here: no tile is read
   if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len) {
     // past the prompt's context: an empty state (max -inf) for each row, so
     // that the merge can fold every chunk slot without knowing the prompt
@@ -419,7 +524,7 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
       for (int rb = 0; rb < RB; ++rb) {
         const int row = row0 + 16 * (RB * rwave + rb) + lr;
         if (row < nrows) {
-          const int64_t slot = (static_cast<int64_t>(slot_k) * p.Nt + qa + row / G) * p.Hq + g * G + row % G;
+          const int64_t slot = (static_cast<int64_t>(slot_k) * p.Nt + qsel[rb]) * p.Hq + g * G + row % G;
           *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, 0.f);
         }
       }
@@ -435,16 +540,16 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
   // this lane's rows: row block rb of row-wave w holds rows 16*(RB*w + rb) + lr
-  // of the unit, row r being question qa + r / G, head g*G + r % G
+  // of the unit, row r being head g*G + r % G of active question qsel (rows
+  // past the active ones read question qa's inputs and are never published)
   int qi[RB], h[RB];
   bool in_range[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int row = row0 + 16 * (RB * rwave + rb) + lr;
     in_range[rb] = row < nrows;
-    const int rr = in_range[rb] ? row : nrows - 1;
-    qi[rb] = qa + rr / G;
-    h[rb] = g * G + rr % G;
+    qi[rb] = in_range[rb] ? qsel[rb] : qa;
+    h[rb] = g * G + row % G;
   }
   // fused instruction unit: each row's query sits at instr_len + ctx_len[b] +
   // seg_len of its own question, b being the prompt (among pa..pe-1) that holds it
@@ -478,22 +583,24 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
 
   bool act[RB];
   bool any_act = false;
+  const bool quad = (G & 3) == 0;                   // lane quads hold heads of one question
   typename M::Frag qf[RB][D / 32];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int s_raw = static_cast<int>(rl.s[rb]);
     act[rb] = in_range[rb] && rl.a[rb] != 0u && usable_seg_len(p, s_raw) >= 0;
     any_act = any_act || act[rb];
-    row_query<T, D, FUSED, RL::QN, (RL::TN > 0 ? RL::TN : 1)>(qf[rb], rl.q[rb], rl.th, row_base[rb] + s_raw);
+    row_query<T, D, FUSED, RL::QN, (RL::TN > 0 ? RL::TN : 1)>(qf[rb], rl.q[rb], rl.th, row_base[rb] + s_raw,
+                                                              quad, lane);
     if (!act[rb]) {
 #pragma unroll
       for (int ds = 0; ds < D / 32; ++ds) qf[rb][ds] = M::zero();
     }
   }
   const bool live = wave_any(any_act);                // wave-uniform
-  // the prologue fills all stages but the PAR that super-iteration 0 fills
+  // the prologue fills every stage of the ring
 #pragma unroll
-  for (int t = P0; t < RG::NS - PAR; ++t)
+  for (int t = P0; t < RG::NS; ++t)
     if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane, toff);
   RowState<D> st[RB];
 #pragma unroll
@@ -503,7 +610,9 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   // ring: tile t sits in stage t % NS.  Super-iteration j covers tiles
   // jP .. jP+P-1 (P = PAR), one per parity; after its barrier the stages of
   // tiles (j-1)P .. jP-1, consumed in super-iteration j-1, are refilled with
-  // tiles jP+NS-P .. jP+NS-1.
+  // tiles jP+NS-P .. jP+NS-1 (for j = 0 the prologue has issued them).
+  // Tiles issued before super-iteration j refills: up to issued(j).
+  auto issued = [](int j) { return j == 0 ? RG::NS - 1 : (j - 1) * PAR + RG::NS - 1; };
   const int last = ntiles - 1;
   const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
   const int my0 = par;                              // this wave's first tile
@@ -520,19 +629,19 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     // the DMA addressing to vector registers.)
     f32x4_t sa[RB][2], sb[RB][2];
     // the first tile of every parity must have landed
-    wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after(RG::NS - PAR - 1, PAR - 1, last));
+    wait_tiles<DPT, RG::NS - PAR>(tiles_after(RG::NS - 1, PAR - 1, last));
     __syncthreads();
     if (live && my0 <= last) qk_tile<T, D, NS, RB>(ring + my0 * RG::STAGE, qf, sa, lr, lg);
     int j = 0;
     // steady state: in super-iterations j and j+1 every parity has a next tile
     for (; (j + 3) * PAR - 1 <= last; j += 2) {
       // super-iteration j: K of tiles up to (j+2)P-1 must have landed
-      wait_tiles<DPT, RG::NS - 3 * PAR>(tiles_after((j - 1) * PAR + RG::NS - 1, (j + 2) * PAR - 1, last));
+      wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after(issued(j), (j + 2) * PAR - 1, last));
       __syncthreads();                              // also: every wave is past super-iteration j-1
 #pragma unroll
       for (int q = 0; q < PAR; ++q) {
         const int tn = j * PAR + RG::NS - PAR + q;
-        if (tn <= last)
+        if (j > 0 && tn <= last)
           issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
       }
       if (live)
@@ -553,12 +662,12 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     // the remaining super-iterations (scores in sa): a parity whose tile has
     // no next tile folds it alone, with the tail mask if it is the last
     for (; j * PAR <= last; ++j) {
-      wait_tiles<DPT, RG::NS - 3 * PAR>(tiles_after((j - 1) * PAR + RG::NS - 1, (j + 2) * PAR - 1, last));
+      wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after(issued(j), (j + 2) * PAR - 1, last));
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < PAR; ++q) {
         const int tn = j * PAR + RG::NS - PAR + q;
-        if (tn <= last)
+        if (j > 0 && tn <= last)
           issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
       }
       const int my = j * PAR + my0, nx = my + PAR;
@@ -578,12 +687,12 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     // one tile per wave per super-iteration, scores and fold together
     for (int j = 0; j * PAR <= last; ++j) {
       // the tiles of super-iteration j must have landed
-      wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after((j - 1) * PAR + RG::NS - 1, (j + 1) * PAR - 1, last));
+      wait_tiles<DPT, RG::NS - PAR>(tiles_after(issued(j), (j + 1) * PAR - 1, last));
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < PAR; ++q) {
         const int tn = j * PAR + RG::NS - PAR + q;
-        if (tn <= last)
+        if (j > 0 && tn <= last)
           issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
       }
       const int my = j * PAR + my0;
@@ -685,7 +794,9 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int hq = g * G + (lr < G ? lr : 0);
   Frag qf[DS];
   T kraw[2], vraw[2];
+  double theta = 0.0;                              // fused: the frequency of pair lane (lanes < D/2)
   if (ww == 0) {
+    if (FUSED) theta = p.inv_freq[lane % (D / 2)];
     const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + hq) * D + lg * 8;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
@@ -719,22 +830,40 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int first = ww < sw ? (ww + sw - 1) % sw : ntiles;
   unsigned char* qrows = sh.main + k * L::TASK;
   const unsigned char* qrow = qrows + lr * L::QROW + lg * 8 * E;
+  // The leader first takes every value its set-up reads from memory (the
+  // rotation at the step token's virtual position ctx_len[b] + seg_len[i],
+  // or the segment's last key and value); then every wave's first tile goes
+  // out, the leader's too, in flight while it rotates and appends the step's
+  // token (cached slots below s do not depend on that append).  The tile
+  // loads are unconditional (a wave without a tile reads slot 0 again), so
+  // that the compiler's waits in the set-up count them on every path instead
+  // of waiting for them.
+  float rcs = 0.f, rsn = 0.f;
+  T lastk[(D + 63) / 64], lastv[(D + 63) / 64];
+  if (ww == 0 && live) {
+    if (FUSED) {
+      const int64_t pos = static_cast<int64_t>(pi.len) + s +
+                          (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
+      if (lane < D / 2) rope_cos_sin(pos, theta, rcs, rsn);
+    } else {
+#pragma unroll
+      for (int r = 0; r < (D + 63) / 64; ++r) {
+        const int d = min(lane + 64 * r, D - 1);
+        lastk[r] = skp[static_cast<int64_t>(s - 1) * D + d];
+        lastv[r] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
+      }
+    }
+  }
   Frag kf[2][DS], vf[DB];
+  load_seg_tile<T, D>(kf, vf, skp, svp, first < ntiles ? first : 0, mlast, lr, lg);
   if (ww == 0) {
     if (lane == 0) sh.live()[k] = live ? 1 : 0;
     if (live) {
-      // query rows of the G heads (rows >= G zero), rotated at the step
-      // token's virtual position ctx_len[b] + seg_len[i] in the fused step
+      // query rows of the G heads (rows >= G zero), rotated in the fused step
       const int h = hq;
       float2* rot = reinterpret_cast<float2*>(qrows + L::QAREA);
       if (FUSED) {
-        const int64_t pos = static_cast<int64_t>(pi.len) + s +
-                            (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
-        for (int jj = lane; jj < D / 2; jj += 64) {
-          float cs, sn;
-          rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
-          rot[jj] = make_float2(cs, sn);
-        }
+        if (lane < D / 2) rot[lane] = make_float2(rcs, rsn);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -786,9 +915,13 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
           }
         }
       } else {
-        for (int d = lane; d < D; d += 64) {
-          sh.k(k)[d] = skp[static_cast<int64_t>(s - 1) * D + d];
-          sh.v(k)[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
+#pragma unroll
+        for (int r = 0; r < (D + 63) / 64; ++r) {
+          const int d = lane + 64 * r;
+          if (d < D) {
+            sh.k(k)[d] = lastk[r];
+            sh.v(k)[d] = lastv[r];
+          }
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -807,8 +940,6 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
       dot = xor32_sum(dot);
       if (lg == 0 && lr < G) sh.slast(k)[lr] = dot;
     }
-  } else if (first < ntiles) {
-    load_seg_tile<T, D>(kf, vf, skp, svp, first, mlast, lr, lg);   // in flight across the barrier
   }
   __syncthreads();                                 // query rows, last keys and their scores are in LDS
 
@@ -817,7 +948,12 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const float c = p.c;
   for (int t = first; t < ntiles; t += sw) {
     asm volatile("" ::: "memory");                // query rows are re-read from LDS, not held in registers
-    if (ww == 0 || t != first) load_seg_tile<T, D>(kf, vf, skp, svp, t, mlast, lr, lg);
+    if (sizeof(T) != 2 && t != first) load_seg_tile<T, D>(kf, vf, skp, svp, t, mlast, lr, lg);
+    // the wave's next tile is in flight while this one is folded (bf16: the
+    // fp32 tiles of two would not fit the registers of the 8-wave units)
+    Frag kn[2][DS], vn[DB];
+    const bool more = sizeof(T) == 2 && t + sw < ntiles;
+    if (more) load_seg_tile<T, D>(kn, vn, skp, svp, t + sw, mlast, lr, lg);
     const int n = min(mem - 32 * t, 32);
     f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
@@ -834,6 +970,14 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
     for (int db = 0; db < DB; ++db) {
       const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
       st.o[db] = M::mma(v, pf, st.o[db]);
+    }
+    if (more) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = kn[kb][ds];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) vf[db] = vn[db];
     }
   }
   __syncthreads();                                 // the query rows are dead

@@ -368,6 +368,26 @@ def test_32layer_sampled(layer):
     check(st, gpu, ref, rec, f"wl5-L{layer}", qsel=sel)
 
 
+def test_32layer_late_steps_every_active_question():
+    """Workload 5 late in its 128 steps, where most questions have stopped and
+    the context units serve only the compacted active rows: every question
+    still active at steps 96 and 127 against the oracle, and the stopped
+    questions' rows left as they were."""
+    st = W.make_structure(W.workload(5))
+    kv = W.layer_kv(st, 0)
+    rec = [96, 127]
+    act = {t: np.flatnonzero(st.active(t)).tolist() for t in rec}
+    log(f"case: workload 5 late steps, active questions {[len(a) for a in act.values()]} of {st.num_questions}")
+    assert 0 < len(act[127]) < len(act[96]) < st.num_questions // 2
+    gpu = run_gpu(st, range(128), rec, kv=kv, fused=True, sentinel=-777.0)
+    assert gpu.err == 0
+    for t in rec:
+        stopped = ~st.active(t)
+        assert np.all(gpu.out[t][stopped] == -777.0) and np.all(gpu.lse[t][stopped] == -777.0)
+    ref = oracle_steps(st, kv, range(128), rec, questions=act)
+    check(st, gpu, ref, rec, "wl5-late", qsel=act)
+
+
 @pytest.mark.parametrize("mode", ["separate", "fused", "standard"])
 def test_maximum_questions_and_group(mode):
     """The documented maxima together: 1024 questions in one prompt (the length
