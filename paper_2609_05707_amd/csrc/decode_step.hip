@@ -392,13 +392,6 @@ struct UnitLds {
   }
 };
 
-// Tiles of a unit (0 .. last) issued after tile `need` while the tiles up
-// to `issued` have gone out: the count a ring wait may leave outstanding.
-__device__ __forceinline__ int tiles_after(int issued, int need, int last) {
-  const int y = min(issued, last) - min(need, last);
-  return y > 0 ? y : 0;
-}
-
 // ---------------------------------------------------------------------------
 // Context unit.  blockIdx -> slice (XCD) = blockIdx & 7, local = blockIdx >> 3;
 // consecutive locals of a slice are the row groups of one chunk (they share
@@ -412,25 +405,13 @@ __device__ __forceinline__ int tiles_after(int issued, int need, int last) {
 // instruction's chunk, and the states go to the instruction slots
 // max_chunks + 1 + chunk.  In the fused step each row's query is rotated at
 // its own question's position instr_len[s] + ctx_len[b] + seg_len[i].
-//
-// PAR > 1: the NW waves are NW / PAR row-waves times PAR tile parities.  All
-// waves of one parity hold the unit's rows between them; parity q folds tiles
-// q, q + PAR, ... of the chunk, so that one workgroup covers PAR times the
-// tokens with the same rows per wave, and the parities' states are combined
-// through LDS before the unit publishes one partial state per row.
-template <typename T, int D, int NW, int NS, bool FUSED, int RB, int PAR, bool INSTR = false>
+template <typename T, int D, int NW, int NS, bool FUSED, int RB, bool INSTR = false>
 __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char* ring, int wave, int lane) {
   using RG = Ring<T, D, NS>;
   using M = Mfma<T>;
   using RL = RowLoads<T, D, FUSED, RB>;
-  static_assert(NW % PAR == 0, "parities must split the waves");
-  constexpr int RWV = NW / PAR;                           // row-waves
-  constexpr int RW = 16 * RB * RWV, DPT = RG::BLOCKS / NW;
-  // tiles issued with the row loads, before the queries are rotated: the
-  // whole ring where the wait count allows
-  constexpr int P0 = RG::NS < 63 / DPT ? RG::NS : 63 / DPT;
-  static_assert(RG::NS >= 2 * PAR && P0 >= 1, "the ring must hold two tiles per parity");
-  const int par = wave / RWV, rwave = wave - par * RWV;   // wave-uniform
+  constexpr int RW = 16 * RB * NW, DPT = RG::BLOCKS / NW;
+  constexpr int P0 = RG::NS - 1 < 3 ? RG::NS - 1 : 3;      // tiles issued before the queries are rotated
   const int lr = lane & 15, lg = lane >> 4;
   // instruction units follow the context units (blockIdx >= ctx_blocks)
   const unsigned ub = INSTR ? blockIdx.x - static_cast<unsigned>(p.ctx_blocks) : blockIdx.x;
@@ -506,6 +487,14 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     slot_k = chunk;
     if (FUSED && p.S > 0) pos_base = instr_pos_base(p.instr_start, p.instr_len, p.S, b);
   }
+  // the prompt's context is split into n = ceil(len / chunk) equal chunks
+  // (whole tiles), so that a short last chunk does not leave its unit idle;
+  // instruction chunks keep the planned size
+  int cb = p.chunk;
+  if (!INSTR && ctx_len > 0) {
+    const int n = (ctx_len + p.chunk - 1) / p.chunk;
+    cb = (((ctx_len + n - 1) / n) + 31) & ~31;
+  }
   const int G = p.G;
   const int row0 = rg * RW;
   if (row0 >= (qb - qa) * G) return;              // beyond every question's rows
@@ -513,16 +502,16 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   // head g*G + r % G of the (r / G)-th active question of [qa, qb)
   int kq[RB], qsel[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) kq[rb] = (row0 + 16 * (RB * rwave + rb) + lr) / G;
+  for (int rb = 0; rb < RB; ++rb) kq[rb] = (row0 + 16 * (RB * wave + rb) + lr) / G;
   const int nrows = active_questions<RB>(p.active, qa, qb, kq, qsel, lane) * G;
   if (row0 >= nrows) return;                       // no active rows here: no tile is read
-  if (static_cast<int64_t>(chunk) * p.chunk >= ctx_len) {
+  if (static_cast<int64_t>(chunk) * cb >= ctx_len) {
     // past the prompt's context: an empty state (max -inf) for each row, so
     // that the merge can fold every chunk slot without knowing the prompt
-    if (lg == 0 && par == 0) {
+    if (lg == 0) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const int row = row0 + 16 * (RB * rwave + rb) + lr;
+        const int row = row0 + 16 * (RB * wave + rb) + lr;
         if (row < nrows) {
           const int64_t slot = (static_cast<int64_t>(slot_k) * p.Nt + qsel[rb]) * p.Hq + g * G + row % G;
           *reinterpret_cast<float2*>(p.part_ml + 2 * slot) = make_float2(-INFINITY, 0.f);
@@ -532,21 +521,21 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     return;
   }
 
-  const int64_t k0 = off + static_cast<int64_t>(chunk) * p.chunk;
-  const int64_t k1 = min(k0 + p.chunk, off + ctx_len);
+  const int64_t k0 = off + static_cast<int64_t>(chunk) * cb;
+  const int64_t k1 = min(k0 + cb, off + ctx_len);
   const int ntiles = static_cast<int>((k1 - k0 + 31) >> 5);
   const T* kbase = static_cast<const T*>(p.ctx_k) + static_cast<int64_t>(g) * p.pool * D;
   const T* vbase = static_cast<const T*>(p.ctx_vt) + static_cast<int64_t>(g) * p.pool * D;
   const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ring));
 
-  // this lane's rows: row block rb of row-wave w holds rows 16*(RB*w + rb) + lr
+  // this lane's rows: row block rb of wave w holds rows 16*(RB*w + rb) + lr
   // of the unit, row r being head g*G + r % G of active question qsel (rows
   // past the active ones read question qa's inputs and are never published)
   int qi[RB], h[RB];
   bool in_range[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int row = row0 + 16 * (RB * rwave + rb) + lr;
+    const int row = row0 + 16 * (RB * wave + rb) + lr;
     in_range[rb] = row < nrows;
     qi[rb] = in_range[rb] ? qsel[rb] : qa;
     h[rb] = g * G + row % G;
@@ -598,151 +587,86 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     }
   }
   const bool live = wave_any(any_act);                // wave-uniform
-  // the prologue fills every stage of the ring
 #pragma unroll
-  for (int t = P0; t < RG::NS; ++t)
+  for (int t = P0; t < RG::NS - 1; ++t)
     if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane, toff);
   RowState<D> st[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) row_init(st[rb]);
   const float c = p.c;
 
-  // ring: tile t sits in stage t % NS.  Super-iteration j covers tiles
-  // jP .. jP+P-1 (P = PAR), one per parity; after its barrier the stages of
-  // tiles (j-1)P .. jP-1, consumed in super-iteration j-1, are refilled with
-  // tiles jP+NS-P .. jP+NS-1 (for j = 0 the prologue has issued them).
-  // Tiles issued before super-iteration j refills: up to issued(j).
-  auto issued = [](int j) { return j == 0 ? RG::NS - 1 : (j - 1) * PAR + RG::NS - 1; };
+  // ring: tile t sits in stage t % NS; at iteration t the stage of tile t-1
+  // is refilled with tile t + NS - 1
   const int last = ntiles - 1;
   const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
-  const int my0 = par;                              // this wave's first tile
-  if constexpr (RG::NS >= 3 * PAR && RG::NS >= 4) {
-    // software pipelined: a wave folds its tile t (softmax on the VALU, then
-    // P^T V on the MFMA) while it computes the scores of its next tile t+P, so
-    // each wave has independent MFMA and VALU work in flight.  K of tiles
-    // jP+P .. jP+2P-1 and V of tiles jP .. jP+P-1 are in the ring during
-    // super-iteration j.  Unrolled by two so that the two score sets (sa,
-    // sb) swap roles instead of being copied; a tile that has no next tile of
-    // its parity (the chunk's last P) is folded alone, with the tail mask.
-    // (Written out rather than as a lambda: a lambda capturing the unit's
-    // bases by reference made the compiler treat them as divergent and move
-    // the DMA addressing to vector registers.)
+  if constexpr (RG::NS >= 4) {
+    // software pipelined: iteration t folds tile t (softmax on the VALU, then
+    // P^T V on the MFMA) while the scores of tile t+1 are computed, so each
+    // wave has independent MFMA and VALU work in flight.  K of tile t+1 and
+    // V of tile t are both in the ring during iteration t.
     f32x4_t sa[RB][2], sb[RB][2];
-    // the first tile of every parity must have landed
-    wait_tiles<DPT, RG::NS - PAR>(tiles_after(RG::NS - 1, PAR - 1, last));
+    // tile 0's blocks are this thread's oldest DMAs; tiles 1 .. min(NS-2, last) are younger
+    wait_tiles<DPT, RG::NS - 2>(min(last, RG::NS - 2));
     __syncthreads();
-    if (live && my0 <= last) qk_tile<T, D, NS, RB>(ring + my0 * RG::STAGE, qf, sa, lr, lg);
-    int j = 0;
-    // steady state: in super-iterations j and j+1 every parity has a next tile
-    for (; (j + 3) * PAR - 1 <= last; j += 2) {
-      // super-iteration j: K of tiles up to (j+2)P-1 must have landed
-      wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after(issued(j), (j + 2) * PAR - 1, last));
-      __syncthreads();                              // also: every wave is past super-iteration j-1
-#pragma unroll
-      for (int q = 0; q < PAR; ++q) {
-        const int tn = j * PAR + RG::NS - PAR + q;
-        if (j > 0 && tn <= last)
-          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
-      }
+    if (live) qk_tile<T, D, NS, RB>(ring, qf, sa, lr, lg);
+    // iteration t < last folds the scores of full tile t and computes those
+    // of tile t+1; unrolled by two so that the two score sets (sa, sb) swap
+    // roles instead of being copied.  The last tile (possibly partial) is
+    // folded after the loop, so the loop carries no masking.  (Written out
+    // rather than as a lambda: a lambda capturing the unit's bases by
+    // reference made the compiler treat them as divergent and move the DMA
+    // addressing to vector registers.)
+    int t = 0;
+    for (; t + 2 <= last; t += 2) {
+      // tile t+1 must have landed; tiles t+2 .. min(t+NS-2, last) are younger
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
+      __syncthreads();                              // also: every wave is past iteration t-1
+      if (t + RG::NS - 1 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 1) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 1), k1, wave, lane, toff);
       if (live)
-        pipe_step<T, D, NS, RB>(ring + (((j + 1) * PAR + my0) % RG::NS) * RG::STAGE,
-                                ring + ((j * PAR + my0) % RG::NS) * RG::STAGE, qf, sa, sb, st, 32, lr, lg, c);
-      wait_tiles<DPT, RG::NS - 3 * PAR>(tiles_after(j * PAR + RG::NS - 1, (j + 3) * PAR - 1, last));
+        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sa, sb,
+                                st, 32, lr, lg, c);
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 2, RG::NS - 3));
       __syncthreads();
-#pragma unroll
-      for (int q = 0; q < PAR; ++q) {
-        const int tn = (j + 1) * PAR + RG::NS - PAR + q;
-        if (tn <= last)
-          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
-      }
+      if (t + RG::NS <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS) % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * (t + RG::NS),
+                                 k1, wave, lane, toff);
       if (live)
-        pipe_step<T, D, NS, RB>(ring + (((j + 2) * PAR + my0) % RG::NS) * RG::STAGE,
-                                ring + (((j + 1) * PAR + my0) % RG::NS) * RG::STAGE, qf, sb, sa, st, 32, lr, lg, c);
+        pipe_step<T, D, NS, RB>(ring + ((t + 2) % RG::NS) * RG::STAGE, ring + ((t + 1) % RG::NS) * RG::STAGE, qf, sb,
+                                sa, st, 32, lr, lg, c);
     }
-    // the remaining super-iterations (scores in sa): a parity whose tile has
-    // no next tile folds it alone, with the tail mask if it is the last
-    for (; j * PAR <= last; ++j) {
-      wait_tiles<DPT, RG::NS - 2 * PAR>(tiles_after(issued(j), (j + 2) * PAR - 1, last));
+    if (t < last) {
+      wait_tiles<DPT, RG::NS - 3>(min(last - t - 1, RG::NS - 3));
       __syncthreads();
-#pragma unroll
-      for (int q = 0; q < PAR; ++q) {
-        const int tn = j * PAR + RG::NS - PAR + q;
-        if (j > 0 && tn <= last)
-          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
+      if (t + RG::NS - 1 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 1) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 1), k1, wave, lane, toff);
+      if (live) {
+        pipe_step<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, ring + (t % RG::NS) * RG::STAGE, qf, sa, sb,
+                                st, 32, lr, lg, c);
+        softmax_pv<T, D, NS, RB>(ring + (last % RG::NS) * RG::STAGE, sb, st, tail_n, lr, lg, c);
       }
-      const int my = j * PAR + my0, nx = my + PAR;
-      if (live && nx <= last) {
-        pipe_step<T, D, NS, RB>(ring + (nx % RG::NS) * RG::STAGE, ring + (my % RG::NS) * RG::STAGE, qf, sa, sb, st, 32,
-                                lr, lg, c);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          sa[rb][0] = sb[rb][0];
-          sa[rb][1] = sb[rb][1];
-        }
-      } else if (live && my <= last) {
-        softmax_pv<T, D, NS, RB>(ring + (my % RG::NS) * RG::STAGE, sa, st, my == last ? tail_n : 32, lr, lg, c);
-      }
+    } else if (live) {
+      softmax_pv<T, D, NS, RB>(ring + (last % RG::NS) * RG::STAGE, sa, st, tail_n, lr, lg, c);
     }
   } else {
-    // one tile per wave per super-iteration, scores and fold together
-    for (int j = 0; j * PAR <= last; ++j) {
-      // the tiles of super-iteration j must have landed
-      wait_tiles<DPT, RG::NS - PAR>(tiles_after(issued(j), (j + 1) * PAR - 1, last));
+    for (int t = 0; t < ntiles; ++t) {
+      // tile t's blocks are this thread's oldest outstanding DMAs; those of
+      // tiles t+1 .. min(t+NS-2, last) are younger
+      wait_tiles<DPT, RG::NS - 2>(min(last - t, RG::NS - 2));
       __syncthreads();
-#pragma unroll
-      for (int q = 0; q < PAR; ++q) {
-        const int tn = j * PAR + RG::NS - PAR + q;
-        if (j > 0 && tn <= last)
-          issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
-      }
-      const int my = j * PAR + my0;
-      if (live && my <= last)
-        ring_tile<T, D, NS, RB>(ring + (my % RG::NS) * RG::STAGE, qf, st, my == last ? tail_n : 32, lr, lg, c);
+      const int tn = t + RG::NS - 1;
+      if (tn <= last)
+        issue_tile<T, D, NW, NS>(lds + (tn % RG::NS) * RG::STAGE, kbase, vbase, k0 + 32ll * tn, k1, wave, lane, toff);
+      if (live) ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, t == last ? tail_n : 32, lr, lg, c);
     }
   }
   wait_vmcnt<0>();                                  // no LDS-DMA may outlive the workgroup
 
-  if constexpr (PAR > 1) {
-    // combine the parities' states lane by lane (the same rows, disjoint tiles)
-    // through LDS, exactly as the merge does: m = max, sums and values rescaled
-    constexpr int SL = D / 4 + 4;                   // floats per lane: values, max, sum (16-byte rows)
-    static_assert((PAR - 1) * RWV * RB * 64 * SL * 4 <= RG::NS * RG::STAGE, "parity states must fit the ring");
-    float* buf = reinterpret_cast<float*>(ring);
-    __syncthreads();                                // every wave is done with the ring
-    if (par > 0 && live) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        float* d = buf + ((((par - 1) * RWV + rwave) * RB + rb) * 64 + lane) * SL;
-#pragma unroll
-        for (int db = 0; db < D / 16; ++db) *reinterpret_cast<f32x4_t*>(d + 4 * db) = st[rb].o[db];
-        *reinterpret_cast<f32x4_t*>(d + D / 4) = f32x4_t{st[rb].m, st[rb].ls[0], 0.f, 0.f};
-      }
-    }
-    __syncthreads();
-    if (par == 0 && live) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        for (int q = 1; q < PAR; ++q) {
-          const float* d = buf + ((((q - 1) * RWV + rwave) * RB + rb) * 64 + lane) * SL;
-          const f32x4_t ml = *reinterpret_cast<const f32x4_t*>(d + D / 4);
-          if (ml[0] == -INFINITY) continue;        // that parity saw no key of this row
-          const float mn = fmaxf(st[rb].m, ml[0]);
-          const float fa = fast_exp2((st[rb].m - mn) * c);   // 0 while this state is empty
-          const float fb = fast_exp2((ml[0] - mn) * c);
-#pragma unroll
-          for (int db = 0; db < D / 16; ++db)
-            st[rb].o[db] = st[rb].o[db] * fa + *reinterpret_cast<const f32x4_t*>(d + 4 * db) * fb;
-          st[rb].ls = st[rb].ls * fa + ml[1] * fb;
-          st[rb].m = mn;
-        }
-      }
-    }
-  }
-  if (par == 0) {
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(slot_k) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
-    }
+  for (int rb = 0; rb < RB; ++rb) {
+    if (act[rb]) publish_rows<D>(p, st[rb], (static_cast<int64_t>(slot_k) * p.Nt + qi[rb]) * p.Hq + h[rb], lg);
   }
 }
 
@@ -794,9 +718,7 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int hq = g * G + (lr < G ? lr : 0);
   Frag qf[DS];
   T kraw[2], vraw[2];
-  double theta = 0.0;                              // fused: the frequency of pair lane (lanes < D/2)
   if (ww == 0) {
-    if (FUSED) theta = p.inv_freq[lane % (D / 2)];
     const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + hq) * D + lg * 8;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
@@ -830,40 +752,22 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int first = ww < sw ? (ww + sw - 1) % sw : ntiles;
   unsigned char* qrows = sh.main + k * L::TASK;
   const unsigned char* qrow = qrows + lr * L::QROW + lg * 8 * E;
-  // The leader first takes every value its set-up reads from memory (the
-  // rotation at the step token's virtual position ctx_len[b] + seg_len[i],
-  // or the segment's last key and value); then every wave's first tile goes
-  // out, the leader's too, in flight while it rotates and appends the step's
-  // token (cached slots below s do not depend on that append).  The tile
-  // loads are unconditional (a wave without a tile reads slot 0 again), so
-  // that the compiler's waits in the set-up count them on every path instead
-  // of waiting for them.
-  float rcs = 0.f, rsn = 0.f;
-  T lastk[(D + 63) / 64], lastv[(D + 63) / 64];
-  if (ww == 0 && live) {
-    if (FUSED) {
-      const int64_t pos = static_cast<int64_t>(pi.len) + s +
-                          (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
-      if (lane < D / 2) rope_cos_sin(pos, theta, rcs, rsn);
-    } else {
-#pragma unroll
-      for (int r = 0; r < (D + 63) / 64; ++r) {
-        const int d = min(lane + 64 * r, D - 1);
-        lastk[r] = skp[static_cast<int64_t>(s - 1) * D + d];
-        lastv[r] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
-      }
-    }
-  }
   Frag kf[2][DS], vf[DB];
-  load_seg_tile<T, D>(kf, vf, skp, svp, first < ntiles ? first : 0, mlast, lr, lg);
   if (ww == 0) {
     if (lane == 0) sh.live()[k] = live ? 1 : 0;
     if (live) {
-      // query rows of the G heads (rows >= G zero), rotated in the fused step
+      // query rows of the G heads (rows >= G zero), rotated at the step
+      // token's virtual position ctx_len[b] + seg_len[i] in the fused step
       const int h = hq;
       float2* rot = reinterpret_cast<float2*>(qrows + L::QAREA);
       if (FUSED) {
-        if (lane < D / 2) rot[lane] = make_float2(rcs, rsn);
+        const int64_t pos = static_cast<int64_t>(pi.len) + s +
+                            (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
+        for (int jj = lane; jj < D / 2; jj += 64) {
+          float cs, sn;
+          rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
+          rot[jj] = make_float2(cs, sn);
+        }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -915,13 +819,9 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
           }
         }
       } else {
-#pragma unroll
-        for (int r = 0; r < (D + 63) / 64; ++r) {
-          const int d = lane + 64 * r;
-          if (d < D) {
-            sh.k(k)[d] = lastk[r];
-            sh.v(k)[d] = lastv[r];
-          }
+        for (int d = lane; d < D; d += 64) {
+          sh.k(k)[d] = skp[static_cast<int64_t>(s - 1) * D + d];
+          sh.v(k)[d] = svp[static_cast<int64_t>((s - 1) >> 3) * 8 * D + d * 8 + ((s - 1) & 7)];
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -940,6 +840,8 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
       dot = xor32_sum(dot);
       if (lg == 0 && lr < G) sh.slast(k)[lr] = dot;
     }
+  } else if (first < ntiles) {
+    load_seg_tile<T, D>(kf, vf, skp, svp, first, mlast, lr, lg);   // in flight across the barrier
   }
   __syncthreads();                                 // query rows, last keys and their scores are in LDS
 
@@ -948,12 +850,7 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const float c = p.c;
   for (int t = first; t < ntiles; t += sw) {
     asm volatile("" ::: "memory");                // query rows are re-read from LDS, not held in registers
-    if (sizeof(T) != 2 && t != first) load_seg_tile<T, D>(kf, vf, skp, svp, t, mlast, lr, lg);
-    // the wave's next tile is in flight while this one is folded (bf16: the
-    // fp32 tiles of two would not fit the registers of the 8-wave units)
-    Frag kn[2][DS], vn[DB];
-    const bool more = sizeof(T) == 2 && t + sw < ntiles;
-    if (more) load_seg_tile<T, D>(kn, vn, skp, svp, t + sw, mlast, lr, lg);
+    if (ww == 0 || t != first) load_seg_tile<T, D>(kf, vf, skp, svp, t, mlast, lr, lg);
     const int n = min(mem - 32 * t, 32);
     f32x4_t sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
@@ -970,14 +867,6 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
     for (int db = 0; db < DB; ++db) {
       const Frag v = n < 32 ? M::keep_first(vf[db], keep) : vf[db];
       st.o[db] = M::mma(v, pf, st.o[db]);
-    }
-    if (more) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = kn[kb][ds];
-#pragma unroll
-      for (int db = 0; db < DB; ++db) vf[db] = vn[db];
     }
   }
   __syncthreads();                                 // the query rows are dead
@@ -1040,14 +929,14 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
 // ---------------------------------------------------------------------------
 // RB = 1: four waves per SIMD (two workgroups per compute unit); RB = 2
 // carries twice the accumulators, at two waves per SIMD.
-template <typename T, int D, int NW, int NS, bool FUSED, int RB, int PAR>
+template <typename T, int D, int NW, int NS, bool FUSED, int RB>
 __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepParams p) {
   __shared__ UnitLds<T, D, NW, NS> sh;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int blk = static_cast<int>(blockIdx.x);
-  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED, RB, PAR>(p, sh.main, wave, lane);
-  else if (blk < p.ctx_blocks + p.instr_blocks) context_unit<T, D, NW, NS, FUSED, RB, PAR, true>(p, sh.main, wave, lane);
+  if (blk < p.ctx_blocks) context_unit<T, D, NW, NS, FUSED, RB>(p, sh.main, wave, lane);
+  else if (blk < p.ctx_blocks + p.instr_blocks) context_unit<T, D, NW, NS, FUSED, RB, true>(p, sh.main, wave, lane);
   else segment_unit<T, D, NW, NS, FUSED>(p, sh, blk - p.ctx_blocks - p.instr_blocks, wave, lane);
 }
 
@@ -1158,10 +1047,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(StepParams p) {
 }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D, int NW, int NS, int RB, int PAR>
+template <typename T, int D, int NW, int NS, int RB>
 static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
-  if (p.fused) attend_kernel<T, D, NW, NS, true, RB, PAR><<<grid, 64 * NW, 0, s>>>(p);
-  else attend_kernel<T, D, NW, NS, false, RB, PAR><<<grid, 64 * NW, 0, s>>>(p);
+  if (p.fused) attend_kernel<T, D, NW, NS, true, RB><<<grid, 64 * NW, 0, s>>>(p);
+  else attend_kernel<T, D, NW, NS, false, RB><<<grid, 64 * NW, 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -1170,46 +1059,41 @@ static hipError_t launch_attend(int grid, const StepParams& p, hipStream_t s) {
 // the chip in one wave, or when registers allow one workgroup per CU anyway.
 // fp32 at D = 128 has 32 KB stages: 2 or 4.  bf16 at D = 128 (16 KB stages)
 // takes the deepest rings the 160 KB of LDS allow: five stages (80 KB, two
-// workgroups per compute unit) or nine (one workgroup).
+// workgroups per compute unit) or nine (one workgroup), so that each compute
+// unit keeps six or seven tiles in flight while it computes.
 template <typename T, int D, int NW, int RB>
 static hipError_t launch_depth(bool deep, int grid, const StepParams& p, hipStream_t s) {
   constexpr int stage = 2 * 32 * D * sizeof(T);
   constexpr int base = stage > 16384 ? 2 : (stage == 16384 ? 5 : 4);
   constexpr int dns = stage > 16384 ? 4 : (stage == 16384 ? 9 : 8);
-  return deep ? launch_attend<T, D, NW, dns, RB, 1>(grid, p, s) : launch_attend<T, D, NW, base, RB, 1>(grid, p, s);
+  return deep ? launch_attend<T, D, NW, dns, RB>(grid, p, s) : launch_attend<T, D, NW, base, RB>(grid, p, s);
 }
 
 template <typename T, int D>
-static hipError_t launch_waves(int waves, int rb, int par, bool deep, int grid, const StepParams& p, hipStream_t s) {
-  if constexpr (sizeof(T) == 2 && D == 128) {
-    // bf16 at D = 128, units of 64 rows and more: one workgroup of eight
-    // waves per compute unit (nine-stage ring), two 16-row blocks per wave,
-    // 8 / par row-waves times par tile parities
-    if (waves == 8 && rb == 2) {
-      if (par == 1) return launch_attend<T, D, 8, 9, 2, 1>(grid, p, s);
-      if (par == 2) return launch_attend<T, D, 8, 9, 2, 2>(grid, p, s);
-      if (par == 4) return launch_attend<T, D, 8, 9, 2, 4>(grid, p, s);
+static hipError_t launch_waves(int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  if (rb == 2) {
+    // two row blocks per wave: bf16 at D = 128 with four or eight waves
+    if constexpr (sizeof(T) == 2 && D == 128) {
+      if (waves == 4) return launch_depth<T, D, 4, 2>(deep, grid, p, s);
+      if (waves == 8) return launch_depth<T, D, 8, 2>(deep, grid, p, s);
     }
-    if (rb == 1 && par == 1 && waves == 1) return launch_depth<T, D, 1, 1>(deep, grid, p, s);
-    if (rb == 1 && par == 1 && waves == 2) return launch_depth<T, D, 2, 1>(deep, grid, p, s);
     return hipErrorInvalidValue;
-  } else {
-    if (rb != 1 || par != 1) return hipErrorInvalidValue;
-    switch (waves) {
-      case 1: return launch_depth<T, D, 1, 1>(deep, grid, p, s);
-      case 2: return launch_depth<T, D, 2, 1>(deep, grid, p, s);
-      case 4: return launch_depth<T, D, 4, 1>(deep, grid, p, s);
-      default:
-        // the planner gives fp32 at D = 128 at most four waves
-        if constexpr (D == 128) return hipErrorInvalidValue;
-        else return launch_depth<T, D, 8, 1>(deep, grid, p, s);
-    }
+  }
+  switch (waves) {
+    case 1: return launch_depth<T, D, 1, 1>(deep, grid, p, s);
+    case 2: return launch_depth<T, D, 2, 1>(deep, grid, p, s);
+    case 4: return launch_depth<T, D, 4, 1>(deep, grid, p, s);
+    default:
+      // the planner gives fp32 at D = 128 at most four waves, and bf16 at
+      // D = 128 eight waves only with two row blocks each
+      if constexpr (D == 128) return hipErrorInvalidValue;
+      else return launch_depth<T, D, 8, 1>(deep, grid, p, s);
   }
 }
 
 template <typename T, int D>
-static hipError_t launch_d(int waves, int rb, int par, bool deep, int grid, const StepParams& p, hipStream_t s) {
-  hipError_t e = launch_waves<T, D>(waves, rb, par, deep, grid, p, s);
+static hipError_t launch_d(int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
+  hipError_t e = launch_waves<T, D>(waves, rb, deep, grid, p, s);
   if (e != hipSuccess) return e;
   merge_kernel<D><<<static_cast<unsigned>(p.Nt) * p.merge_parts, kMergeThreads, 0, s>>>(p);
   return hipGetLastError();
@@ -1222,14 +1106,12 @@ hipError_t launch_merge(const StepParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_step(int dtype, int waves, int rb, int par, bool deep, int grid, const StepParams& p,
-                       hipStream_t s) {
+hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s) {
   if (p.Nt == 0 || grid == 0) return hipSuccess;
   if (dtype == 0)
-    return p.D == 64 ? launch_d<float, 64>(waves, rb, par, deep, grid, p, s)
-                     : launch_d<float, 128>(waves, rb, par, deep, grid, p, s);
-  return p.D == 64 ? launch_d<uint16_t, 64>(waves, rb, par, deep, grid, p, s)
-                   : launch_d<uint16_t, 128>(waves, rb, par, deep, grid, p, s);
+    return p.D == 64 ? launch_d<float, 64>(waves, rb, deep, grid, p, s) : launch_d<float, 128>(waves, rb, deep, grid, p, s);
+  return p.D == 64 ? launch_d<uint16_t, 64>(waves, rb, deep, grid, p, s)
+                   : launch_d<uint16_t, 128>(waves, rb, deep, grid, p, s);
 }
 
 }  // namespace ippd

@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "ippd.h"
@@ -103,25 +104,15 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
     if (want > sized_rows) sized_rows = want;
   }
   if (rows == 0) rows = sized_rows <= 16 ? 16 : (sized_rows <= 32 ? 32 : (sized_rows <= 64 ? 64 : (sized_rows <= 128 || !two_blocks_ok ? 128 : 256)));
-  // dense-mask units: 16 * rb rows per wave, no parities
-  int dense_rb = rows > 64 && two_blocks_ok ? 2 : 1;
-  int dense_waves = rows / (16 * dense_rb);
+  const int rb = rows > 64 && two_blocks_ok ? 2 : 1;
+  int waves = rows / (16 * rb);
   // fp32 at D = 128: the operands of eight waves do not fit their registers
-  if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && dense_waves > 4) dense_waves = 4;
-  int rb = dense_rb, waves = dense_waves, par = 1;
-  if (two_blocks_ok && rows >= 64) {
-    // bf16 at D = 128: one workgroup of eight waves per compute unit, two
-    // 16-row blocks per wave; units of 256, 128 or 64 rows are 8, 4 or 2
-    // row-waves times 1, 2 or 4 tile parities
-    rb = 2;
-    waves = 8;
-    par = 256 / rows;
-  }
-  const int unit_rows = 16 * rb * waves / par;
+  if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && waves > 4) waves = 4;
+  const int unit_rows = 16 * rb * waves;
   const int nrg = static_cast<int>((max_rows + unit_rows - 1) / unit_rows);
   // workgroups resident per compute unit (eight waves of two row blocks use
   // the registers of two, and their ring the LDS of one)
-  const int wg_per_cu = dense ? ((dense_rb == 2 && dense_waves == 8) ? 1 : 2) : ((rb == 2 && waves == 8) ? 1 : 2);
+  const int wg_per_cu = (rb == 2 && waves == 8) ? 1 : 2;
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   // two-level batch: instruction groups, (instruction, kv head) or (question, kv head)
@@ -131,7 +122,13 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   const int nrg_i = S == 0 ? 1 : static_cast<int>((irows + unit_rows - 1) / unit_rows);
   int chunk = bt->chunk_tokens;
   if (chunk == 0) {
-    const int64_t work = n_groups * nrg * bt->max_ctx_len + n_igroups * nrg_i * (S ? bt->max_instr_len : 0);
+    // context tokens to stream: one-level IPPD reads each prompt once, and the
+    // prompts are packed in the pool, so its size bounds their sum (a ragged
+    // batch then gets a chunk from its total, not from B times the longest)
+    const int64_t ctx_tokens = shared ? std::min<int64_t>(bt->ctx_pool_tokens,
+                                                          static_cast<int64_t>(bt->num_prompts) * bt->max_ctx_len)
+                                      : static_cast<int64_t>(bt->num_questions) * bt->max_ctx_len;
+    const int64_t work = ctx_tokens * bt->num_kv_heads * nrg + n_igroups * nrg_i * (S ? bt->max_instr_len : 0);
     const int64_t target = static_cast<int64_t>(compute_units()) * wg_per_cu;
     int64_t ch = (work + target - 1) / target;
     ch = (ch + 31) / 32 * 32;
@@ -163,10 +160,8 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   const int64_t grid = ctx_blocks + instr_blocks + seg_blocks;
   if (grid > (1ll << 30) || n_groups * max_chunks > (1ll << 30) || n_igroups * max_ichunks > (1ll << 30)) return false;
   pl->shared = shared ? 1 : 0;
-  pl->waves = dense ? dense_waves : waves;
-  pl->rb = dense ? dense_rb : rb;
-  pl->par = dense ? 1 : par;
-  pl->dense_waves = dense_waves;
+  pl->waves = waves;
+  pl->rb = rb;
   pl->nrg = nrg;
   pl->chunk = chunk;
   pl->max_chunks = static_cast<int>(max_chunks);
@@ -255,7 +250,7 @@ ippd_status_t decode(const ippd_batch_t* bt, bool shared, bool fused, const void
   p.dense = pl.dense;
   fill_inv_freq(bt, p.inv_freq);
   if (pl.dense) return hip_status(ippd::launch_dense(bt->dtype, pl.waves, pl.rb, pl.grid, p, stream));
-  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.par, pl.deep != 0, pl.grid, p, stream));
+  return hip_status(ippd::launch_step(bt->dtype, pl.waves, pl.rb, pl.deep != 0, pl.grid, p, stream));
 }
 
 

@@ -54,9 +54,6 @@ struct StepPlan {
   int shared;              // 1: IPPD, context units serve all questions of a prompt
   int waves;               // waves per workgroup; a context unit covers 16 * rb rows per wave
   int rb;                  // 16-row blocks per wave (1, or 2 for bf16 at D = 128)
-  int par;                 // tile parities: waves / par row-waves share the unit's rows, parity q
-                           // folding tiles q, q + par, ... of the chunk (bf16 at D = 128)
-  int dense_waves;         // waves per dense-mask unit (16 * rb rows each, no parities)
   int nrg;                 // row groups per group
   int chunk;               // context tokens per context unit (multiple of 32)
   int max_chunks;          // ceil(max_ctx_len / chunk)
@@ -138,8 +135,7 @@ struct StepParams {
 hipError_t launch_load_context(int dtype, const LoadContextParams& p, hipStream_t s);
 hipError_t launch_load_segments(int dtype, const LoadSegmentsParams& p, hipStream_t s);
 hipError_t launch_append(int dtype, const AppendParams& p, hipStream_t s);
-hipError_t launch_step(int dtype, int waves, int rb, int par, bool deep, int grid, const StepParams& p,
-                       hipStream_t s);
+hipError_t launch_step(int dtype, int waves, int rb, bool deep, int grid, const StepParams& p, hipStream_t s);
 // merge_kernel alone (the dense-mask baseline's second launch)
 hipError_t launch_merge(const StepParams& p, hipStream_t s);
 // dense-mask baseline: dense_kernel (context-chunk units, then dense segment

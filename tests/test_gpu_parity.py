@@ -91,6 +91,25 @@ def test_small_ragged(dtype, d, chunk, rows, fused):
                                   st.seg_len_at(st.wl.steps))
 
 
+@pytest.mark.parametrize("mode", ["fused", "separate", "standard"])
+def test_more_than_64_prompts(mode):
+    """80 ragged prompts: the prompt lookups take their second window of 64
+    (segment units, standard context units, the append kernel), and the
+    pool-sized chunk splits the longer contexts into equal chunks.  Every
+    question against the oracle over two steps with stops after the first."""
+    log(f"case: 80 prompts, mode={mode}")
+    wl = W.custom_workload(wid=270, dtype="bf16", num_prompts=80, hq=8, hkv=2, head_dim=128,
+                           ctx_len=(24, 400), questions=(1, 3), seg_len=(1, 30), steps=2, stop=(1, 2))
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0, 1], [0, 1], kv=kv, fused=mode != "separate", standard=mode == "standard")
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, [0, 1], [0, 1])
+    check(st, gpu, ref, [0, 1], f"80-prompts-{mode}")
+    if mode != "standard":
+        np.testing.assert_array_equal(gpu.batch.seg_len[0][: st.num_questions].cpu().numpy(), st.seg_len_at(2))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_fused_step_equals_separate_calls(dtype):
     """ippd_decode_step == ippd_append_kv + ippd_decode_attention (same rotation, same
