@@ -58,6 +58,9 @@ def parse():
                     help="question-steps the oracle computes (default: 400, 240 on the 32-layer workload)")
     ap.add_argument("--chunk", type=int, default=0, help="context tokens per unit (0 = library default)")
     ap.add_argument("--tile-rows", type=int, default=0, help="rows per context unit (0 = library default)")
+    ap.add_argument("--standard-only", action="store_true",
+                    help="profiling aid: run only the standard baseline's timed steps (no JSON line); its "
+                         "kernels are then the only decode kernels a counter run sees")
     return ap.parse_args()
 
 
@@ -115,10 +118,11 @@ def dense_flops(st: W.Structure, t: int) -> int:
     return tot
 
 
-def read_traffic(workload_id: int):
-    """HBM traffic per attention launch from the committed rocprofv3 counter summary,
+def read_traffic(workload_id: int, path_kind: str = "decode"):
+    """HBM traffic per attention launch from the committed rocprofv3 counter summary
+    (path_kind "decode": the IPPD step, "standard": the standard baseline's step),
     only if it was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_decode_step_wl{workload_id}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_{path_kind}_step_wl{workload_id}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -304,6 +308,11 @@ def main():
         durs = [a.elapsed_time(b) / 1e3 for row in ev for (a, b) in row]
         return float(np.mean(durs)), durs
 
+    if args.standard_only:
+        t_std = timed(True)
+        print(f"standard only: {t_std / (steps * layers) * 1e6:.3f} us per layer-step, err flag {db.err_flag()}",
+              file=sys.stderr)
+        return
     t_ippd = timed(False)
     err = db.err_flag()
     tokens = sum(int(st.active(t % data_steps).sum()) for t in range(steps)) * layers
@@ -417,6 +426,8 @@ def main():
             # algorithmic-bytes rate (re-reads may be served from L2 or the
             # Infinity Cache), not HBM bandwidth
             "algorithmic_bytes_rate_gbps": round(float(np.mean(std_b)) / ks_avg / 1e9, 1),
+            # HBM bytes per call from FETCH_SIZE + WRITE_SIZE counters (null if not taken on these sources)
+            "traffic": read_traffic(wl.wid, "standard"),
         }
     if not args.no_dense and db.ws_dense_bytes > 0:
         # the paper's own scheme (dense mask over the whole stacked prompt), as
