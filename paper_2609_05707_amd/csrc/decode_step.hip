@@ -599,7 +599,11 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
   // is refilled with tile t + NS - 1
   const int last = ntiles - 1;
   const int tail_n = static_cast<int>(k1 - (k0 + 32ll * last));
-  if constexpr (RG::NS >= 4) {
+  // eight single-block waves at bf16, D = 128 (one workgroup per compute
+  // unit): the plain loop, whose waves overlap each other's MFMA and VALU
+  // work, measured faster than the pipelined one
+  constexpr bool kPipelined = RG::NS >= 4 && !(NW == 8 && RB == 1 && D == 128 && sizeof(T) == 2);
+  if constexpr (kPipelined) {
     // software pipelined: iteration t folds tile t (softmax on the VALU, then
     // P^T V on the MFMA) while the scores of tile t+1 are computed, so each
     // wave has independent MFMA and VALU work in flight.  K of tile t+1 and
@@ -1085,8 +1089,10 @@ static hipError_t launch_waves(int waves, int rb, bool deep, int grid, const Ste
     case 4: return launch_depth<T, D, 4, 1>(deep, grid, p, s);
     default:
       // the planner gives fp32 at D = 128 at most four waves, and bf16 at
-      // D = 128 eight waves only with two row blocks each
-      if constexpr (D == 128) return hipErrorInvalidValue;
+      // D = 128 eight single-block waves only with one workgroup per compute
+      // unit (the deep ring)
+      if constexpr (D == 128 && sizeof(T) == 4) return hipErrorInvalidValue;
+      else if constexpr (D == 128) return launch_attend<T, D, 8, 9, 1>(grid, p, s);
       else return launch_depth<T, D, 8, 1>(deep, grid, p, s);
   }
 }

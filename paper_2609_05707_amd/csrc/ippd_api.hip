@@ -104,7 +104,15 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
     if (want > sized_rows) sized_rows = want;
   }
   if (rows == 0) rows = sized_rows <= 16 ? 16 : (sized_rows <= 32 ? 32 : (sized_rows <= 64 ? 64 : (sized_rows <= 128 || !two_blocks_ok ? 128 : 256)));
-  const int rb = rows > 64 && two_blocks_ok ? 2 : 1;
+  // 128-row units at bf16, D = 128 over prompts of (nearly) one length: eight
+  // waves of one 16-row block each, one workgroup per compute unit with the
+  // deep ring.  Half the units of the four-wave shape (two workgroups per
+  // compute unit), so half the partial states, at the same streaming rate;
+  // ragged batches keep the four-wave shape, whose second workgroup per
+  // compute unit covers the uneven unit lengths.
+  const bool near_uniform = bt->ctx_pool_tokens * 10 >= static_cast<int64_t>(bt->num_prompts) * bt->max_ctx_len * 9;
+  const bool eight_single = two_blocks_ok && shared && !dense && bt->num_instr == 0 && rows == 128 && near_uniform;
+  const int rb = rows > 64 && two_blocks_ok && !eight_single ? 2 : 1;
   int waves = rows / (16 * rb);
   // fp32 at D = 128: the operands of eight waves do not fit their registers
   if (bt->dtype == IPPD_DTYPE_F32 && bt->head_dim == 128 && waves > 4) waves = 4;
@@ -112,7 +120,7 @@ bool plan_step(const ippd_batch_t* bt, bool shared, ippd::StepPlan* pl, bool den
   const int nrg = static_cast<int>((max_rows + unit_rows - 1) / unit_rows);
   // workgroups resident per compute unit (eight waves of two row blocks use
   // the registers of two, and their ring the LDS of one)
-  const int wg_per_cu = (rb == 2 && waves == 8) ? 1 : 2;
+  const int wg_per_cu = (waves == 8 && (rb == 2 || eight_single)) ? 1 : 2;
   const int64_t n_groups = shared ? static_cast<int64_t>(bt->num_prompts) * bt->num_kv_heads
                                   : static_cast<int64_t>(bt->num_questions) * bt->num_kv_heads;
   // two-level batch: instruction groups, (instruction, kv head) or (question, kv head)
