@@ -722,7 +722,9 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
   const int hq = g * G + (lr < G ? lr : 0);
   Frag qf[DS];
   T kraw[2], vraw[2];
+  double theta = 0.0;                              // fused: frequency of pair `lane` (lanes < D/2)
   if (ww == 0) {
+    if (FUSED) theta = p.inv_freq[lane % (D / 2)];   // loaded with the row, not after the prompt lookup
     const T* src = static_cast<const T*>(FUSED ? p.q_new : p.q_rot_in) + (static_cast<int64_t>(i) * p.Hq + hq) * D + lg * 8;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[ds] = M::load(src + 32 * ds);
@@ -767,10 +769,10 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
       if (FUSED) {
         const int64_t pos = static_cast<int64_t>(pi.len) + s +
                             (p.S > 0 ? instr_pos_base(p.instr_start, p.instr_len, p.S, pi.b) : 0);
-        for (int jj = lane; jj < D / 2; jj += 64) {
+        if (lane < D / 2) {
           float cs, sn;
-          rope_cos_sin(pos, p.inv_freq[jj], cs, sn);
-          rot[jj] = make_float2(cs, sn);
+          rope_cos_sin(pos, theta, cs, sn);
+          rot[lane] = make_float2(cs, sn);
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
