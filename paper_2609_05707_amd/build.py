@@ -18,6 +18,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libippd.so")
 
 SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip", "prefill.hip", "dense_mask.hip"]
+# standalone measurement programs, built next to the library
+TOOLS = {"stream_ceiling.hip": os.path.join(HERE, "stream_ceiling")}
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -58,11 +60,23 @@ def _compile(src: str, extra) -> str:
     return obj
 
 
+def _tool(src: str, exe: str) -> str:
+    cmd = [hipcc(), *flags_for(src), os.path.join(CSRC, src), "-o", exe]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    return exe
+
+
 def build(verbose: bool = False, extra_flags=()) -> str:
-    """Compile every HIP source for gfx950 and link libippd.so next to this file."""
+    """Compile every HIP source for gfx950 and link libippd.so next to this file
+    (and the standalone measurement programs beside it)."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+    with ThreadPoolExecutor(max_workers=len(SOURCES) + len(TOOLS)) as ex:
+        tools = [ex.submit(_tool, src, exe) for src, exe in TOOLS.items()]
         objs = list(ex.map(lambda s: _compile(s, list(extra_flags)), SOURCES))
+        for f in tools:
+            f.result()
     tmp = LIB_PATH + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -12,7 +12,8 @@ the five wait states the hardware needs after a vector instruction writes
 those SGPRs; a base moved there by v_readfirstlane just before the asm was
 read stale and sent a tile DMA to a wild address.  The asm therefore waits
 them out itself (s_nop 4); the DMA tests check that every SGPR-base DMA of
-the three kernel sources does, and that no base is left in VGPRs."""
+the kernel sources (and of the streaming-ceiling program) does, and that
+no base is left in VGPRs."""
 import os
 import re
 import shutil
@@ -185,7 +186,7 @@ def test_dma_hazard_scan_flags_planted_cases():
 
 @pytest.mark.skipif(shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"),
                     reason="hipcc not available")
-@pytest.mark.parametrize("src", ["prefill.hip", "dense_mask.hip"])
+@pytest.mark.parametrize("src", ["prefill.hip", "dense_mask.hip", "stream_ceiling.hip"])
 def test_dma_bases_in_sgprs_with_wait_states(tmp_path, src):
     out = tmp_path / (src + ".s")
     flags = [f for f in B.flags_for(src) if f != "-fPIC"]
