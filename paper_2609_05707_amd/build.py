@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libippd.so")
 
 SOURCES = ["ippd_api.hip", "rope_append.hip", "decode_step.hip", "prefill.hip", "dense_mask.hip"]
 # standalone measurement programs, built next to the library
-TOOLS = {"stream_ceiling.hip": os.path.join(HERE, "stream_ceiling")}
+TOOLS = {"stream_ceiling.hip": os.path.join(HERE, "stream_ceiling"), "l2_handoff.hip": os.path.join(HERE, "l2_handoff")}
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
