@@ -933,8 +933,9 @@ __device__ __forceinline__ void segment_unit(const StepParams& p, UnitLds<T, D, 
 // Workgroups are dispatched in order, so segment units start as context
 // units retire and fill the tail of the context work.
 // ---------------------------------------------------------------------------
-// RB = 1: four waves per SIMD (two workgroups per compute unit); RB = 2
-// carries twice the accumulators, at two waves per SIMD.
+// The second launch bound asks for four waves per SIMD with one row block
+// per wave and two with RB = 2 (twice the accumulators); the ring's LDS then
+// sets the workgroups per compute unit: one with nine stages, two with five.
 template <typename T, int D, int NW, int NS, bool FUSED, int RB>
 __global__ __launch_bounds__(64 * NW, RB == 1 ? 4 : 2) void attend_kernel(StepParams p) {
   __shared__ UnitLds<T, D, NW, NS> sh;

@@ -24,11 +24,29 @@ from collections import defaultdict
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def kernel_source_hash() -> str:
+KERNEL_SOURCES = ("decode_step.hip", "tile_attend.h", "ippd_device.h", "ippd_internal.h", "ippd_api.hip")
+
+
+def code_only(text: str) -> str:
+    """Source text without comments, blank lines or layout: what a counter
+    record's fingerprint covers (a comment or layout edit leaves the kernels,
+    and so their counters, as they were)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    lines = []
+    for line in text.splitlines():
+        line = line.split("//", 1)[0].strip()
+        if line:
+            lines.append(" ".join(line.split()))
+    return "\n".join(lines)
+
+
+def kernel_source_hash(csrc: str = os.path.join(ROOT, "paper_2609_05707_amd", "csrc")) -> str:
+    """Fingerprint of the decode kernels' code, stored with each counter
+    record; bench.py uses a record only while the sources still match it."""
     h = hashlib.sha256()
-    for f in ("decode_step.hip", "tile_attend.h", "ippd_device.h", "ippd_internal.h", "ippd_api.hip"):
-        with open(os.path.join(ROOT, "paper_2609_05707_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -67,3 +67,23 @@ def test_prefill_flops_by_hand():
     q_i = (3 * 15 + 3 * 4 // 2) + (4 * 15 + 4 * 5 // 2)
     assert BP.flops(st, False, ins) == per * (ins_rows + ctx_i + q_i)
     assert BP.flops(st, True, ins) == per * (2 * ins_rows + 2 * ctx_i + q_i)
+
+
+def test_counter_fingerprint_ignores_comments_but_not_code(tmp_path):
+    """A counter record stays valid across comment and layout edits of the
+    kernel sources, and not across a code change."""
+    import shutil
+    from paper_2609_05707_amd import traffic as T
+    src = os.path.join(ROOT, "paper_2609_05707_amd", "csrc")
+    for f in T.KERNEL_SOURCES:
+        shutil.copy(os.path.join(src, f), tmp_path / f)
+    h0 = T.kernel_source_hash(str(tmp_path))
+    assert h0 == T.kernel_source_hash(src)
+    k = tmp_path / "decode_step.hip"
+    text = k.read_text()
+    k.write_text("// a new comment line\n/* and a block\n   comment */\n" + text.replace("\n", "  \n\n", 3) +
+                 "\n// trailing\n")
+    assert T.kernel_source_hash(str(tmp_path)) == h0
+    k.write_text(text.replace("constexpr int kMergeBatch = 8;", "constexpr int kMergeBatch = 4;"))
+    assert "constexpr int kMergeBatch = 8;" in text
+    assert T.kernel_source_hash(str(tmp_path)) != h0
