@@ -40,8 +40,9 @@ __device__ __forceinline__ void rotate8(const T* __restrict__ src, T* __restrict
 // (VE = 16 bytes / element size, VG = D / VE).  Every load is issued before
 // the question's state is known; the prompt is found with one ballot over
 // the prompts (lane l reads prompt l), so a question costs one round trip of
-// loads and then its stores.  Rotations use the same cos/sin and rounding as
-// the fused decode step, so both give identical bits.
+// loads and then its stores.  The D/2 (cos, sin) pairs of the question's
+// position are evaluated once, into LDS; rotations use the same cos/sin and
+// rounding as the fused decode step, so both give identical bits.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(1024) void append_kernel(AppendParams p) {
@@ -55,20 +56,11 @@ __global__ __launch_bounds__(1024) void append_kernel(AppendParams p) {
   // the thread's items (a block covers a question in one pass when it can)
   constexpr int kMaxPass = 2;
   vec_t lo[kMaxPass], hi[kMaxPass];
-  // theta of the item's VE pairs, read with 16-byte loads before anything
-  // else: one round trip, where per-pair reads of the parameter block would
-  // each wait for the last
-  typedef double th_t __attribute__((ext_vector_type(2)));
-  th_t th[kMaxPass][VE / 2];
-#pragma unroll
-  for (int r = 0; r < kMaxPass; ++r) {
-    const int e = threadIdx.x + r * blockDim.x;
-    const int ee = e < nq ? e : e - nq;
-    const int j0 = e < nq + nk ? (ee % QP) * VE : 0;
-    const th_t* tp = reinterpret_cast<const th_t*>(p.inv_freq + j0);
-#pragma unroll
-    for (int u = 0; u < VE / 2; ++u) th[r][u] = tp[u];
-  }
+  // every head of the question turns by the same D/2 angles: thread j < D/2
+  // evaluates pair j's once into LDS (its frequency read first, with the
+  // other loads, so that it shares their round trip)
+  __shared__ float2 rot[kMaxHalfDim];
+  const double theta = threadIdx.x < static_cast<unsigned>(half) ? p.inv_freq[threadIdx.x] : 0.0;
   // the question's state, and the first 64 prompts' question ends and
   // context lengths for the prompt lookup below, all loaded before any wait
   const bool act = p.active[i] != 0;
@@ -124,6 +116,12 @@ __global__ __launch_bounds__(1024) void append_kernel(AppendParams p) {
     return;
   }
   const int64_t pos = instr_pos_base(p.instr_start, p.instr_len, p.S, b) + len + s;
+  if (threadIdx.x < static_cast<unsigned>(half)) {
+    float c, sn;
+    rope_cos_sin(pos, theta, c, sn);
+    rot[threadIdx.x] = make_float2(c, sn);
+  }
+  __syncthreads();                                 // act and s are the question's: every thread is here
   T* __restrict__ qr = static_cast<T*>(p.q_rot);
   T* __restrict__ sk = static_cast<T*>(p.seg_k);
   T* __restrict__ svt = static_cast<T*>(p.seg_vt);
@@ -137,9 +135,9 @@ __global__ __launch_bounds__(1024) void append_kernel(AppendParams p) {
       vec_t x, y;
 #pragma unroll
       for (int u = 0; u < VE; ++u) {
-        float c, sn, xr, yr;
-        rope_cos_sin(pos, th[r][u / 2][u & 1], c, sn);
-        rope_rotate(to_f32<T>(lo[r][u]), to_f32<T>(hi[r][u]), c, sn, xr, yr);
+        const float2 cs = rot[j0 + u];
+        float xr, yr;
+        rope_rotate(to_f32<T>(lo[r][u]), to_f32<T>(hi[r][u]), cs.x, cs.y, xr, yr);
         x[u] = from_f32<T>(xr);
         y[u] = from_f32<T>(yr);
       }
