@@ -30,14 +30,30 @@ KERNEL_SOURCES = ("decode_step.hip", "tile_attend.h", "ippd_device.h", "ippd_int
 def code_only(text: str) -> str:
     """Source text without comments, blank lines or layout: what a counter
     record's fingerprint covers (a comment or layout edit leaves the kernels,
-    and so their counters, as they were)."""
-    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-    lines = []
-    for line in text.splitlines():
-        line = line.split("//", 1)[0].strip()
-        if line:
-            lines.append(" ".join(line.split()))
-    return "\n".join(lines)
+    and so their counters, as they were).  String and character literals are
+    kept whole, so a "//" or "/*" inside one is code."""
+    out = []
+    i, n = 0, len(text)
+    while i < n:
+        ch = text[i]
+        if ch in "\"'":
+            j = i + 1
+            while j < n and text[j] != ch:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            while i < n and text[i] != "\n":
+                i += 1
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(ch)
+            i += 1
+    lines = (" ".join(line.split()) for line in "".join(out).splitlines())
+    return "\n".join(line for line in lines if line)
 
 
 def kernel_source_hash(csrc: str = os.path.join(ROOT, "paper_2609_05707_amd", "csrc")) -> str:

@@ -87,3 +87,6 @@ def test_counter_fingerprint_ignores_comments_but_not_code(tmp_path):
     k.write_text(text.replace("constexpr int kMergeBatch = 8;", "constexpr int kMergeBatch = 4;"))
     assert "constexpr int kMergeBatch = 8;" in text
     assert T.kernel_source_hash(str(tmp_path)) != h0
+    # a "//" inside a string literal is code, not a comment
+    assert T.code_only('asm("a // b");  // note') == 'asm("a // b");'
+    assert T.code_only("x = '/'; /* c */ y = 1;") == "x = '/'; y = 1;"
