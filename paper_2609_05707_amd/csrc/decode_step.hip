@@ -587,8 +587,12 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
     }
   }
   const bool live = wave_any(any_act);                // wave-uniform
+  // the eight-wave plain loop folds two tiles per barrier (below): its ring
+  // starts one tile shallower, so that the stages it refills are the two
+  // whose tiles every wave has folded
+  constexpr bool kPairs = RG::NS >= 6 && NW == 8 && RB == 1 && D == 128 && sizeof(T) == 2;
 #pragma unroll
-  for (int t = P0; t < RG::NS - 1; ++t)
+  for (int t = P0; t < RG::NS - (kPairs ? 2 : 1); ++t)
     if (t < ntiles) issue_tile<T, D, NW, NS>(lds + t * RG::STAGE, kbase, vbase, k0 + 32ll * t, k1, wave, lane, toff);
   RowState<D> st[RB];
 #pragma unroll
@@ -653,6 +657,34 @@ __device__ __forceinline__ void context_unit(const StepParams& p, unsigned char*
       }
     } else if (live) {
       softmax_pv<T, D, NS, RB>(ring + (last % RG::NS) * RG::STAGE, sa, st, tail_n, lr, lg, c);
+    }
+  } else if constexpr (kPairs) {
+    // two tiles per barrier: at iteration t (even) tiles t and t+1 have
+    // landed and every wave has folded tiles t-2 and t-1, whose stages take
+    // tiles t+NS-2 and t+NS-1; an odd last tile is folded on its own.
+    // Half the barriers, so half the waits for the slowest wave (measured
+    // 0.4% faster than one tile per barrier on the 32-layer workload).
+    int t = 0;
+    for (; t + 1 < ntiles; t += 2) {
+      // tiles t+2 .. min(t+NS-4, last) are younger than tile t+1
+      wait_tiles<DPT, RG::NS - 4>(min(last - t - 1, RG::NS - 4));
+      __syncthreads();
+      if (t + RG::NS - 2 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 2) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 2), k1, wave, lane, toff);
+      if (t + RG::NS - 1 <= last)
+        issue_tile<T, D, NW, NS>(lds + ((t + RG::NS - 1) % RG::NS) * RG::STAGE, kbase, vbase,
+                                 k0 + 32ll * (t + RG::NS - 1), k1, wave, lane, toff);
+      if (live) {
+        ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, 32, lr, lg, c);
+        ring_tile<T, D, NS, RB>(ring + ((t + 1) % RG::NS) * RG::STAGE, qf, st, t + 1 == last ? tail_n : 32, lr, lg,
+                                c);
+      }
+    }
+    if (t == last) {
+      wait_tiles<DPT, RG::NS - 4>(0);
+      __syncthreads();
+      if (live) ring_tile<T, D, NS, RB>(ring + (t % RG::NS) * RG::STAGE, qf, st, tail_n, lr, lg, c);
     }
   } else {
     for (int t = 0; t < ntiles; ++t) {
