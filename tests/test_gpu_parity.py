@@ -91,6 +91,27 @@ def test_small_ragged(dtype, d, chunk, rows, fused):
                                   st.seg_len_at(st.wl.steps))
 
 
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("ctx,chunk", [(37, 0), (200, 0), (200, 64), (200, 96), (300, 96)])
+def test_eight_wave_units_odd_and_short_tile_counts(ctx, chunk, fused):
+    """Prompts of one context length with 32 questions of G = 4 heads: the
+    planner's eight single-block waves per 128-row unit, whose loop folds two
+    tiles per barrier.  Context lengths and chunk sizes give units of 1, 2, 3,
+    7 and 10 tiles (odd counts fold their last tile alone, units shorter than
+    the ring start with a partial prologue), partial last tiles, and a second
+    step after some questions stopped."""
+    log(f"case: eight-wave units ctx={ctx} chunk={chunk} fused={fused}")
+    wl = W.custom_workload(wid=280, dtype="bf16", num_prompts=2, hq=32, hkv=8, head_dim=128,
+                           ctx_len=(ctx, ctx), questions=(32, 32), question_tokens=0, seg_len=(1, 40),
+                           steps=2, stop=(1, 2))
+    st = W.make_structure(wl)
+    kv = W.layer_kv(st)
+    gpu = run_gpu(st, [0, 1], [0, 1], chunk_tokens=chunk, kv=kv, fused=fused)
+    assert gpu.err == 0
+    ref = oracle_steps(st, kv, [0, 1], [0, 1])
+    check(st, gpu, ref, [0, 1], f"eight-wave-{ctx}-{chunk}-{'fused' if fused else 'sep'}")
+
+
 @pytest.mark.parametrize("mode", ["fused", "separate", "standard"])
 def test_more_than_64_prompts(mode):
     """80 ragged prompts: the prompt lookups take their second window of 64
